@@ -1,0 +1,352 @@
+"""Thin ctypes binding of libpipeboost.so (argument marshalling only).
+
+Every step of the prefill runs inside the HIP library.  PyTorch is used only
+to allocate the device arena and the two streams.  There is no fallback: if
+the library is missing, loading fails with an error.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "lib", "libpipeboost.so")
+
+PB_OK, PB_EINVAL, PB_ENOTPINNED, PB_ENOMEM, PB_EHIP, PB_ESTATE = 0, -1, -2, -3, -4, -5
+PB_BF16, PB_F16 = 0, 1
+LORA_BITS = {"q": 1, "k": 2, "v": 4, "o": 8}
+TARGET_INDEX = {"q": 0, "k": 1, "v": 2, "o": 3}
+LAYER_TENSOR_ID = {n: i for i, n in enumerate(
+    ("ln1_g", "ln1_b", "wq", "bq", "wk", "bk", "wv", "bv", "wo", "bo", "ln2_g", "ln2_b",
+     "w1", "b1", "w2", "b2"))}
+GLOBAL_TENSOR_ID = {"embed": 0, "pos": 1, "lnf_g": 2, "lnf_b": 3}
+KERNEL_KINDS = ("embed", "layernorm", "lora_shrink", "gemm_qkv", "attention", "gemm_o",
+                "gemm_fc1", "gemm_fc2", "lm_head", "argmax")
+
+
+class PbError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__("pipeboost error %d: %s" % (code, msg))
+        self.code = code
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("d_ffn", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("max_pos", ctypes.c_int32),
+                ("max_tokens", ctypes.c_int32), ("max_batch", ctypes.c_int32),
+                ("max_adapters", ctypes.c_int32), ("max_rank", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("ln_eps", ctypes.c_float)]
+
+
+_SIGS = {
+    "pb_layer_bytes": (ctypes.c_size_t, [ctypes.POINTER(Config)]),
+    "pb_globals_bytes": (ctypes.c_size_t, [ctypes.POINTER(Config)]),
+    "pb_layer_tensor": (ctypes.c_int, [ctypes.POINTER(Config), ctypes.c_int32,
+                                       ctypes.POINTER(ctypes.c_size_t),
+                                       ctypes.POINTER(ctypes.c_size_t)]),
+    "pb_globals_tensor": (ctypes.c_int, [ctypes.POINTER(Config), ctypes.c_int32,
+                                         ctypes.POINTER(ctypes.c_size_t),
+                                         ctypes.POINTER(ctypes.c_size_t)]),
+    "pb_lora_layer_bytes": (ctypes.c_size_t, [ctypes.POINTER(Config), ctypes.c_int32,
+                                              ctypes.c_uint32]),
+    "pb_lora_tensor": (ctypes.c_int, [ctypes.POINTER(Config), ctypes.c_int32, ctypes.c_uint32,
+                                      ctypes.c_int32, ctypes.c_int32,
+                                      ctypes.POINTER(ctypes.c_size_t),
+                                      ctypes.POINTER(ctypes.c_size_t)]),
+    "pb_arena_bytes": (ctypes.c_size_t, [ctypes.POINTER(Config)]),
+    "pb_host_alloc": (ctypes.c_int, [ctypes.c_size_t, ctypes.POINTER(ctypes.c_void_p)]),
+    "pb_host_free": (ctypes.c_int, [ctypes.c_void_p]),
+    "pb_model_create": (ctypes.c_int, [ctypes.POINTER(Config), ctypes.c_void_p, ctypes.c_size_t,
+                                       ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.POINTER(ctypes.c_void_p)]),
+    "pb_stream_layers": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32),
+                                        ctypes.c_int32, ctypes.POINTER(ctypes.c_void_p),
+                                        ctypes.c_void_p]),
+    "pb_attach_lora": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                      ctypes.c_float, ctypes.c_uint32,
+                                      ctypes.POINTER(ctypes.c_void_p)]),
+    "pb_prefill_first_token": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32),
+                                              ctypes.c_int32, ctypes.c_int32,
+                                              ctypes.POINTER(ctypes.c_int32),
+                                              ctypes.POINTER(ctypes.c_int32),
+                                              ctypes.POINTER(ctypes.c_float)]),
+    "pb_destroy": (ctypes.c_int, [ctypes.c_void_p]),
+    "pb_last_error": (ctypes.c_char_p, []),
+    "pb_set_chunk_bytes": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t]),
+    "pb_last_load_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_double),
+                                          ctypes.POINTER(ctypes.c_double)]),
+    "pb_set_kernel_timing": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
+    "pb_get_kernel_timing": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32,
+                                            ctypes.POINTER(ctypes.c_double),
+                                            ctypes.POINTER(ctypes.c_int64)]),
+    "pb_reset_kernel_timing": (ctypes.c_int, [ctypes.c_void_p]),
+    "pb_poison_weights": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
+    "pb_set_stream_delay_us": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
+}
+
+_lib = None
+
+
+def lib():
+    """Load libpipeboost.so (built by ``paper_2503_17707_amd.build``); raise if absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libpipeboost.so is not built (%s); run __graft_entry__.build()"
+                               % LIB_PATH)
+        # One HIP runtime per process: torch ships its own libamdhip64.so.7 with
+        # the same soname, so it must be loaded first and the library then binds
+        # to it (the streams torch creates are only valid in that runtime).
+        import torch  # noqa: F401
+
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def check(rc: int) -> None:
+    if rc != PB_OK:
+        raise PbError(rc, lib().pb_last_error().decode())
+
+
+def make_config(w, max_tokens: Optional[int] = None, max_batch: Optional[int] = None,
+                max_adapters: Optional[int] = None, max_rank: Optional[int] = None) -> Config:
+    """pb_config of a synth.Workload (capacities default to the workload's own sizes)."""
+    return Config(n_layers=w.n_layers, d_model=w.d_model, n_heads=w.n_heads, d_ffn=w.d_ffn,
+                  vocab=w.vocab, max_pos=w.max_pos,
+                  max_tokens=max_tokens or w.batch * w.seq_len,
+                  max_batch=max_batch or w.batch,
+                  max_adapters=w.n_adapters if max_adapters is None else max_adapters,
+                  max_rank=max_rank or w.lora_rank,
+                  dtype=PB_BF16 if w.dtype == "bf16" else PB_F16, ln_eps=w.ln_eps)
+
+
+def layer_tensor(cfg: Config, name: str):
+    off, n = ctypes.c_size_t(), ctypes.c_size_t()
+    check(lib().pb_layer_tensor(ctypes.byref(cfg), LAYER_TENSOR_ID[name], ctypes.byref(off),
+                                ctypes.byref(n)))
+    return off.value, n.value
+
+
+def globals_tensor(cfg: Config, name: str):
+    off, n = ctypes.c_size_t(), ctypes.c_size_t()
+    check(lib().pb_globals_tensor(ctypes.byref(cfg), GLOBAL_TENSOR_ID[name], ctypes.byref(off),
+                                  ctypes.byref(n)))
+    return off.value, n.value
+
+
+def lora_tensor(cfg: Config, rank: int, mask: int, target: str, which: str):
+    off, n = ctypes.c_size_t(), ctypes.c_size_t()
+    check(lib().pb_lora_tensor(ctypes.byref(cfg), rank, mask, TARGET_INDEX[target],
+                               0 if which == "A" else 1, ctypes.byref(off), ctypes.byref(n)))
+    return off.value, n.value
+
+
+class Pinned:
+    """A pinned host buffer from pb_host_alloc, freed with pb_host_free."""
+
+    def __init__(self, nbytes: int):
+        p = ctypes.c_void_p()
+        check(lib().pb_host_alloc(nbytes, ctypes.byref(p)))
+        self.ptr = p.value
+        self.nbytes = nbytes
+
+    def view(self, dtype=np.uint8) -> np.ndarray:
+        buf = (ctypes.c_uint8 * self.nbytes).from_address(self.ptr)
+        return np.frombuffer(buf, dtype=np.uint8).view(dtype)
+
+    def free(self):
+        if self.ptr:
+            lib().pb_host_free(self.ptr)
+            self.ptr = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+class HostWeights:
+    """Pinned host blobs of a workload in the library's device layout, drawn by synth."""
+
+    def __init__(self, w, cfg: Config):
+        import synth
+
+        self.w, self.cfg = w, cfg
+        L = lib()
+        kind = w.dtype
+        self.layer_bytes = L.pb_layer_bytes(ctypes.byref(cfg))
+        self.globals_bytes = L.pb_globals_bytes(ctypes.byref(cfg))
+        if not self.layer_bytes or not self.globals_bytes:
+            raise PbError(PB_EINVAL, "invalid config for %s" % w.name)
+        self.globals = Pinned(self.globals_bytes)
+        self.globals.view()[:] = 0
+        for name in synth.GLOBAL_TENSORS:
+            off, _ = globals_tensor(cfg, name)
+            synth.fill_base_tensor(w, -1, name, kind, self.globals.ptr + 2 * off)
+        self.layers: List[Pinned] = []
+        for layer in range(w.n_layers):
+            blob = Pinned(self.layer_bytes)
+            self._zero_padding(blob, cfg)
+            for name in synth.LAYER_TENSORS:
+                off, _ = layer_tensor(cfg, name)
+                synth.fill_base_tensor(w, layer, name, kind, blob.ptr + 2 * off)
+            self.layers.append(blob)
+        self.loras: Dict[int, List[Pinned]] = {}
+
+    def _zero_padding(self, blob: Pinned, cfg: Config):
+        # every byte of the blob is written by a tensor except alignment gaps
+        ctypes.memset(blob.ptr, 0, blob.nbytes)
+
+    def lora_mask(self) -> int:
+        m = 0
+        for t in self.w.lora_targets:
+            m |= LORA_BITS[t]
+        return m
+
+    def add_lora(self, adapter: int) -> List[Pinned]:
+        import synth
+
+        w, cfg = self.w, self.cfg
+        mask = self.lora_mask()
+        nbytes = lib().pb_lora_layer_bytes(ctypes.byref(cfg), w.lora_rank, mask)
+        if not nbytes:
+            raise PbError(PB_EINVAL, "invalid LoRA shape")
+        blobs = []
+        for layer in range(w.n_layers):
+            blob = Pinned(nbytes)
+            for t in w.lora_targets:
+                for which in ("A", "B"):
+                    off, _ = lora_tensor(cfg, w.lora_rank, mask, t, which)
+                    synth.fill_lora_tensor(w, adapter, layer, t, which, w.dtype,
+                                           blob.ptr + 2 * off)
+            blobs.append(blob)
+        self.loras[adapter] = blobs
+        return blobs
+
+    def free(self):
+        self.globals.free()
+        for b in self.layers:
+            b.free()
+        for bl in self.loras.values():
+            for b in bl:
+                b.free()
+
+
+class Model:
+    """A pb_model over a torch-allocated arena and two torch streams."""
+
+    def __init__(self, cfg: Config, device: str = "cuda:0"):
+        import torch
+
+        self.cfg = cfg
+        L = lib()
+        self.arena_bytes = L.pb_arena_bytes(ctypes.byref(cfg))
+        if not self.arena_bytes:
+            raise PbError(PB_EINVAL, "invalid config")
+        self.device = torch.device(device)
+        self.arena = torch.empty(self.arena_bytes + 256, dtype=torch.uint8, device=self.device)
+        base = self.arena.data_ptr()
+        self.base = (base + 255) // 256 * 256
+        self.copy_stream = torch.cuda.Stream(device=self.device)
+        self.compute_stream = torch.cuda.Stream(device=self.device)
+        torch.cuda.synchronize(self.device)
+        h = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            check(L.pb_model_create(ctypes.byref(cfg), ctypes.c_void_p(self.base),
+                                    self.arena_bytes, ctypes.c_void_p(self.copy_stream.cuda_stream),
+                                    ctypes.c_void_p(self.compute_stream.cuda_stream),
+                                    ctypes.byref(h)))
+        self.h = h
+
+    def stream_layers(self, hw: HostWeights, order: Optional[Sequence[int]] = None):
+        n = self.cfg.n_layers
+        order = list(range(n)) if order is None else list(order)
+        arr = (ctypes.c_int32 * len(order))(*order)
+        ptrs = (ctypes.c_void_p * n)(*[b.ptr for b in hw.layers])
+        check(lib().pb_stream_layers(self.h, arr, len(order), ptrs, ctypes.c_void_p(hw.globals.ptr)))
+
+    def attach_lora(self, slot: int, blobs: List[Pinned], rank: int, alpha: float, mask: int):
+        ptrs = (ctypes.c_void_p * len(blobs))(*[b.ptr for b in blobs])
+        check(lib().pb_attach_lora(self.h, slot, rank, alpha, mask, ptrs))
+
+    def prefill(self, tokens: np.ndarray, adapter_of_seq: Optional[Sequence[int]] = None,
+                want_logits: bool = True):
+        tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+        B, T = tokens.shape
+        out_tok = np.empty(B, dtype=np.int32)
+        logits = np.empty((B, self.cfg.vocab), dtype=np.float32) if want_logits else None
+        ad = None
+        if adapter_of_seq is not None:
+            ad_arr = np.ascontiguousarray(adapter_of_seq, dtype=np.int32)
+            ad = ad_arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        check(lib().pb_prefill_first_token(
+            self.h, tokens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), B, T, ad,
+            out_tok.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+            logits.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if want_logits else None))
+        return out_tok, logits
+
+    def poison(self, value: int = 0xFF):
+        check(lib().pb_poison_weights(self.h, value))
+
+    def set_chunk_bytes(self, n: int):
+        check(lib().pb_set_chunk_bytes(self.h, n))
+
+    def set_stream_delay_us(self, us: int):
+        check(lib().pb_set_stream_delay_us(self.h, us))
+
+    def load_stats(self):
+        b, ms = ctypes.c_double(), ctypes.c_double()
+        check(lib().pb_last_load_stats(self.h, ctypes.byref(b), ctypes.byref(ms)))
+        return b.value, ms.value
+
+    def set_timing(self, on: bool):
+        check(lib().pb_set_kernel_timing(self.h, 1 if on else 0))
+
+    def reset_timing(self):
+        check(lib().pb_reset_kernel_timing(self.h))
+
+    def timing(self) -> Dict[str, tuple]:
+        out = {}
+        for i, k in enumerate(KERNEL_KINDS):
+            ms, n = ctypes.c_double(), ctypes.c_int64()
+            check(lib().pb_get_kernel_timing(self.h, i, ctypes.byref(ms), ctypes.byref(n)))
+            out[k] = (ms.value, n.value)
+        return out
+
+    def destroy(self):
+        if self.h:
+            lib().pb_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+def setup(w, device: str = "cuda:0", hw: Optional[HostWeights] = None, **cap):
+    """Create host blobs (pinned), a model, and attach the workload's adapters (slots 0..)."""
+    cfg = make_config(w, **cap)
+    hw = hw or HostWeights(w, cfg)
+    m = Model(cfg, device)
+    return hw, m
+
+
+def attach_all(m: Model, hw: HostWeights):
+    """Attach adapter a of the workload into slot a, for every adapter it uses."""
+    w = hw.w
+    used = sorted({a for a in w.adapters() if a >= 0})
+    for a in used:
+        blobs = hw.loras.get(a) or hw.add_lora(a)
+        m.attach_lora(a, blobs, w.lora_rank, w.lora_alpha, hw.lora_mask())

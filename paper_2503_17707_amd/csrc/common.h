@@ -1,0 +1,60 @@
+// Device-side helpers shared by the CDNA4 (gfx950) kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pb {
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// Storage-type traits: T is _Float16 or __bf16.
+template <typename T> struct Mfma;
+
+template <> struct Mfma<_Float16> {
+    typedef f16x8 vec8;
+    // D[16x16] += A[16x32] B[32x16]; lane l holds A row l%16, k = 8(l/16)..+7,
+    // B column l%16, k = 8(l/16)..+7, and D rows 4(l/16)+i, column l%16.
+    __device__ static inline f32x4 mma(vec8 a, vec8 b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+    }
+};
+
+template <> struct Mfma<__bf16> {
+    typedef bf16x8 vec8;
+    __device__ static inline f32x4 mma(vec8 a, vec8 b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+};
+
+template <typename T> __device__ inline float to_f32(T x) { return (float)x; }
+template <typename T> __device__ inline T from_f32(float x) { return (T)x; }
+
+// Reinterpret 16 bytes as the MFMA operand vector of T.
+template <typename T> __device__ inline typename Mfma<T>::vec8 as_vec8(u32x4 v) {
+    return __builtin_bit_cast(typename Mfma<T>::vec8, v);
+}
+
+// Pack 4 floats into 4 storage-type values (8 bytes), round to nearest even.
+template <typename T> __device__ inline u32x2 pack4(float a, float b, float c, float d) {
+    T t[4] = {(T)a, (T)b, (T)c, (T)d};
+    u32x2 r;
+    __builtin_memcpy(&r, t, 8);
+    return r;
+}
+
+__device__ inline float wave_sum(float v) {
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+__device__ inline float wave_max(float v) {
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+}  // namespace pb

@@ -1,0 +1,306 @@
+// Memory-bound kernels of the prefill: embedding, LayerNorm, LM head, argmax
+// and the LoRA slot packing.  All read and write with 16-byte vectors.
+#include "common.h"
+#include "kernels.h"
+
+namespace pb {
+
+namespace {
+
+// ---- embedding: OPT learned absolute positions, no offset -------------------
+template <typename T>
+__global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ tok,
+                                                   const T* __restrict__ E,
+                                                   const T* __restrict__ P,
+                                                   float* __restrict__ x, int T_len, int d) {
+    const int row = blockIdx.x;
+    const int t = row % T_len;
+    const T* e = E + (int64_t)tok[row] * d;
+    const T* pp = P + (int64_t)t * d;
+    float* xr = x + (int64_t)row * d;
+    for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
+        const u32x4 ev = *(const u32x4*)(e + c);
+        const u32x4 pv = *(const u32x4*)(pp + c);
+        T ea[8], pa[8];
+        __builtin_memcpy(ea, &ev, 16);
+        __builtin_memcpy(pa, &pv, 16);
+        f32x4 lo, hi;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            lo[i] = (float)ea[i] + (float)pa[i];
+            hi[i] = (float)ea[4 + i] + (float)pa[4 + i];
+        }
+        *(f32x4*)(xr + c) = lo;
+        *(f32x4*)(xr + c + 4) = hi;
+    }
+}
+
+// ---- LayerNorm: one 256-thread block per row, values kept in registers ------
+constexpr int LN_MAXC = 16;  // float4 chunks per thread: d <= 256 * 4 * 16
+
+__device__ __forceinline__ float block_sum(float v, float* red) {
+    v = wave_sum(v);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    __syncthreads();
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    return red[0] + red[1] + red[2] + red[3];
+}
+
+template <typename T, bool OUT_F32>
+__global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict__ x,
+                                                       int64_t in_mul, int64_t in_add,
+                                                       const T* __restrict__ g,
+                                                       const T* __restrict__ b, void* out,
+                                                       int d, float eps) {
+    __shared__ float red[4];
+    const int row = blockIdx.x;
+    const float* xr = x + ((int64_t)row * in_mul + in_add) * d;
+    const int nc = d / 4;
+    f32x4 v[LN_MAXC];
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < LN_MAXC; ++i) {
+        const int c = threadIdx.x + 256 * i;
+        if (c < nc) {
+            v[i] = *(const f32x4*)(xr + 4 * c);
+            s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
+        }
+    }
+    const float mean = block_sum(s, red) / (float)d;
+    float q = 0.f;
+#pragma unroll
+    for (int i = 0; i < LN_MAXC; ++i) {
+        const int c = threadIdx.x + 256 * i;
+        if (c < nc) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float t = v[i][r] - mean;
+                q += t * t;
+            }
+        }
+    }
+    const float var = block_sum(q, red) / (float)d;
+    const float rstd = 1.0f / sqrtf(var + eps);
+#pragma unroll
+    for (int i = 0; i < LN_MAXC; ++i) {
+        const int c = threadIdx.x + 256 * i;
+        if (c < nc) {
+            const u32x2 graw = *(const u32x2*)(g + 4 * c);
+            const u32x2 braw = *(const u32x2*)(b + 4 * c);
+            T ga[4], ba[4];
+            __builtin_memcpy(ga, &graw, 8);
+            __builtin_memcpy(ba, &braw, 8);
+            float y[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) y[r] = (v[i][r] - mean) * rstd * (float)ga[r] + (float)ba[r];
+            if (OUT_F32) {
+                *(f32x4*)((float*)out + (int64_t)row * d + 4 * c) = f32x4{y[0], y[1], y[2], y[3]};
+            } else {
+                *(u32x2*)((T*)out + (int64_t)row * d + 4 * c) = pack4<T>(y[0], y[1], y[2], y[3]);
+            }
+        }
+    }
+}
+
+// ---- LM head: logits[b, v] = z[b] . E[v], one wave per 8 vocabulary rows ----
+constexpr int LM_ROWS = 8;
+constexpr int LM_NB = 4;  // sequences per pass
+
+template <typename T>
+__global__ __launch_bounds__(256) void lm_head_kernel(const float* __restrict__ z, int B,
+                                                     const T* __restrict__ E, int V, int d,
+                                                     float* __restrict__ logits) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int v0 = (blockIdx.x * 4 + wave) * LM_ROWS;
+    if (v0 >= V) return;
+    for (int b0 = 0; b0 < B; b0 += LM_NB) {
+        const int nb = min(LM_NB, B - b0);
+        float acc[LM_ROWS][LM_NB];
+#pragma unroll
+        for (int r = 0; r < LM_ROWS; ++r)
+#pragma unroll
+            for (int j = 0; j < LM_NB; ++j) acc[r][j] = 0.f;
+        for (int c = lane * 8; c < d; c += 64 * 8) {
+            float zb[LM_NB][8];
+#pragma unroll
+            for (int j = 0; j < LM_NB; ++j) {
+                if (j < nb) {
+                    const f32x4 a = *(const f32x4*)(z + (int64_t)(b0 + j) * d + c);
+                    const f32x4 bq = *(const f32x4*)(z + (int64_t)(b0 + j) * d + c + 4);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        zb[j][e] = a[e];
+                        zb[j][4 + e] = bq[e];
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) zb[j][e] = 0.f;
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < LM_ROWS; ++r) {
+                const int v = min(v0 + r, V - 1);
+                const u32x4 ev = *(const u32x4*)(E + (int64_t)v * d + c);
+                T ea[8];
+                __builtin_memcpy(ea, &ev, 16);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float w = (float)ea[e];
+#pragma unroll
+                    for (int j = 0; j < LM_NB; ++j) acc[r][j] += w * zb[j][e];
+                }
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < LM_ROWS; ++r)
+#pragma unroll
+            for (int j = 0; j < LM_NB; ++j) {
+                const float t = wave_sum(acc[r][j]);
+                if (lane == 0 && j < nb && v0 + r < V) logits[(int64_t)(b0 + j) * V + v0 + r] = t;
+            }
+    }
+}
+
+// ---- argmax: one block per sequence, lowest index among equal maxima --------
+__global__ __launch_bounds__(1024) void argmax_kernel(const float* __restrict__ logits, int V,
+                                                     int32_t* __restrict__ tok) {
+    __shared__ float sv[16];
+    __shared__ int si[16];
+    const int b = blockIdx.x;
+    const float* l = logits + (int64_t)b * V;
+    float best = -INFINITY;
+    int bi = 0x7fffffff;
+    for (int v = threadIdx.x; v < V; v += 1024) {
+        const float x = l[v];
+        if (x > best || (x == best && v < bi)) {
+            best = x;
+            bi = v;
+        }
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+        const float ov = __shfl_xor(best, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (ov > best || (ov == best && oi < bi)) {
+            best = ov;
+            bi = oi;
+        }
+    }
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) {
+        sv[wave] = best;
+        si[wave] = bi;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float bb = sv[0];
+        int ii = si[0];
+        for (int w = 1; w < 16; ++w)
+            if (sv[w] > bb || (sv[w] == bb && si[w] < ii)) {
+                bb = sv[w];
+                ii = si[w];
+            }
+        tok[b] = (ii == 0x7fffffff || !(bb > -INFINITY)) ? -1 : ii;
+    }
+}
+
+// ---- LoRA slot packing -----------------------------------------------------
+// grid (L, 4 targets, 2 parts); part 0 writes Acat[l][t][slot*rs + j][:],
+// part 1 writes Bcat[l][t][n][slot*rs + j].
+template <typename T>
+__global__ __launch_bounds__(256) void lora_pack_kernel(const T* __restrict__ staging,
+                                                       size_t staging_layer_elems, int d, int r,
+                                                       uint32_t mask, int slot, int rs, int kw,
+                                                       T* __restrict__ Acat,
+                                                       T* __restrict__ Bcat) {
+    const int l = blockIdx.x, t = blockIdx.y, part = blockIdx.z;
+    const bool present = (mask >> t) & 1u;
+    // position of target t in the staged blob: targets before it that are present
+    int idx = 0;
+    for (int u = 0; u < t; ++u) idx += (mask >> u) & 1u;
+    const T* A = staging + (size_t)l * staging_layer_elems + (size_t)idx * 2 * r * d;
+    const T* Bm = A + (size_t)r * d;
+    const T zero = (T)0.f;
+    if (part == 0) {
+        T* dst = Acat + ((size_t)l * 4 + t) * (size_t)kw * d + (size_t)slot * rs * d;
+        for (int i = threadIdx.x; i < rs * d; i += 256) {
+            const int j = i / d;
+            dst[i] = (present && j < r) ? A[i] : zero;
+        }
+    } else {
+        T* dst = Bcat + ((size_t)l * 4 + t) * (size_t)d * kw + (size_t)slot * rs;
+        for (int i = threadIdx.x; i < d * rs; i += 256) {
+            const int n = i / rs, j = i % rs;
+            dst[(size_t)n * kw + j] = (present && j < r) ? Bm[(size_t)n * r + j] : zero;
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_embed(int dtype, const int32_t* tok, const void* E, const void* P, float* x,
+                        int n_rows, int T_len, int d, hipStream_t s) {
+    if (n_rows <= 0) return hipSuccess;
+    if (dtype == 1)
+        hipLaunchKernelGGL(embed_kernel<_Float16>, dim3(n_rows), dim3(256), 0, s, tok,
+                           (const _Float16*)E, (const _Float16*)P, x, T_len, d);
+    else
+        hipLaunchKernelGGL(embed_kernel<__bf16>, dim3(n_rows), dim3(256), 0, s, tok,
+                           (const __bf16*)E, (const __bf16*)P, x, T_len, d);
+    return hipGetLastError();
+}
+
+hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t in_add,
+                            const void* g, const void* b, void* out, bool out_f32, int rows,
+                            int d, float eps, hipStream_t s) {
+    if (rows <= 0) return hipSuccess;
+    if (d % 4 || d > 256 * 4 * LN_MAXC) return hipErrorInvalidValue;
+#define PB_LN(T, F)                                                                            \
+    hipLaunchKernelGGL((layernorm_kernel<T, F>), dim3(rows), dim3(256), 0, s, x, in_mul, in_add, \
+                       (const T*)g, (const T*)b, out, d, eps)
+    if (dtype == 1) {
+        if (out_f32) PB_LN(_Float16, true); else PB_LN(_Float16, false);
+    } else {
+        if (out_f32) PB_LN(__bf16, true); else PB_LN(__bf16, false);
+    }
+#undef PB_LN
+    return hipGetLastError();
+}
+
+hipError_t launch_lm_head(int dtype, const float* z, int B, const void* E, int V, int d,
+                          float* logits, hipStream_t s) {
+    if (B <= 0 || V <= 0) return hipSuccess;
+    if (d % 8) return hipErrorInvalidValue;
+    const int blocks = (V + 4 * LM_ROWS - 1) / (4 * LM_ROWS);
+    if (dtype == 1)
+        hipLaunchKernelGGL(lm_head_kernel<_Float16>, dim3(blocks), dim3(256), 0, s, z, B,
+                           (const _Float16*)E, V, d, logits);
+    else
+        hipLaunchKernelGGL(lm_head_kernel<__bf16>, dim3(blocks), dim3(256), 0, s, z, B,
+                           (const __bf16*)E, V, d, logits);
+    return hipGetLastError();
+}
+
+hipError_t launch_argmax(const float* logits, int B, int V, int32_t* tok, hipStream_t s) {
+    if (B <= 0) return hipSuccess;
+    hipLaunchKernelGGL(argmax_kernel, dim3(B), dim3(1024), 0, s, logits, V, tok);
+    return hipGetLastError();
+}
+
+hipError_t launch_lora_pack(int dtype, const void* staging, size_t staging_layer_elems, int L,
+                            int d, int r, uint32_t mask, int slot, int rs, int kw, void* Acat,
+                            void* Bcat, hipStream_t s) {
+    if (L <= 0) return hipSuccess;
+    dim3 grid(L, 4, 2);
+    if (dtype == 1)
+        hipLaunchKernelGGL(lora_pack_kernel<_Float16>, grid, dim3(256), 0, s,
+                           (const _Float16*)staging, staging_layer_elems, d, r, mask, slot, rs, kw,
+                           (_Float16*)Acat, (_Float16*)Bcat);
+    else
+        hipLaunchKernelGGL(lora_pack_kernel<__bf16>, grid, dim3(256), 0, s, (const __bf16*)staging,
+                           staging_layer_elems, d, r, mask, slot, rs, kw, (__bf16*)Acat,
+                           (__bf16*)Bcat);
+    return hipGetLastError();
+}
+
+}  // namespace pb

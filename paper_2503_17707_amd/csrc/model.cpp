@@ -1,0 +1,733 @@
+// Host runtime of the cold-start prefill: layout, loader, forward scheduler
+// and the C ABI declared in include/pipeboost.h.
+//
+// Loading overlaps inference (PipeBoost, Sections 4.2 and 4.3): the loader
+// enqueues each layer's host-to-device copies on the copy stream and records
+// one event per layer; the forward pass enqueues every layer's kernels on the
+// compute stream behind hipStreamWaitEvent(compute, event[layer]).  Waiting
+// happens on the device, so the host enqueues the whole forward at once and
+// layer l starts the moment its bytes have landed, while later layers are
+// still crossing PCIe.  The compute schedule (kernel sequence, tiling,
+// reduction orders) never depends on the load order, so results are
+// bit-identical for any order.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "../../include/pipeboost.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+#define HIP_TRY(call)                                                                  \
+    do {                                                                               \
+        hipError_t e_ = (call);                                                        \
+        if (e_ != hipSuccess)                                                          \
+            return fail(PB_EHIP, "%s failed: %s (%s:%d)", #call, hipGetErrorString(e_), \
+                        __FILE__, __LINE__);                                           \
+    } while (0)
+
+constexpr size_t ALIGN = 256;
+constexpr int MAX_SLOTS = 16;
+constexpr int MAX_RANK = 64;
+constexpr size_t VEC_ALIGN = 128;  // elements (256 bytes of dt)
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool config_ok(const pb_config* c, std::string* why) {
+    auto bad = [&](const char* m) {
+        if (why) *why = m;
+        return false;
+    };
+    if (!c) return bad("config is NULL");
+    if (c->n_layers < 1) return bad("n_layers must be >= 1");
+    if (c->d_model < 128 || c->d_model % 128) return bad("d_model must be a positive multiple of 128");
+    if (c->d_model > 16384) return bad("d_model must be <= 16384");
+    if (c->n_heads < 1 || c->d_model % c->n_heads) return bad("n_heads must divide d_model");
+    const int hd = c->d_model / c->n_heads;
+    if (hd != 64 && hd != 128) return bad("head_dim must be 64 or 128");
+    if (c->d_ffn < 64 || c->d_ffn % 64) return bad("d_ffn must be a positive multiple of 64");
+    if (c->vocab < 1) return bad("vocab must be >= 1");
+    if (c->max_pos < 1) return bad("max_pos must be >= 1");
+    if (c->max_tokens < 1 || c->max_batch < 1) return bad("max_tokens and max_batch must be >= 1");
+    if (c->max_adapters < 0 || c->max_adapters > MAX_SLOTS) return bad("max_adapters must be in [0, 16]");
+    if (c->max_adapters > 0 && (c->max_rank < 1 || c->max_rank > MAX_RANK))
+        return bad("max_rank must be in [1, 64]");
+    if (c->dtype != PB_BF16 && c->dtype != PB_F16) return bad("dtype must be PB_BF16 or PB_F16");
+    if (!(c->ln_eps > 0.f)) return bad("ln_eps must be > 0");
+    return true;
+}
+
+struct LayerLayout {
+    size_t off[PB_T_COUNT];
+    size_t num[PB_T_COUNT];
+    size_t total;  // elements
+};
+
+LayerLayout layer_layout(const pb_config* c) {
+    const size_t d = c->d_model, f = c->d_ffn;
+    LayerLayout L{};
+    size_t p = 0;
+    auto put = [&](int t, size_t n, bool align) {
+        if (align) p = align_up(p, VEC_ALIGN);
+        L.off[t] = p;
+        L.num[t] = n;
+        p += n;
+    };
+    put(PB_T_WQ, d * d, true);
+    put(PB_T_WK, d * d, false);
+    put(PB_T_WV, d * d, false);
+    put(PB_T_WO, d * d, true);
+    put(PB_T_W1, f * d, true);
+    put(PB_T_W2, d * f, true);
+    put(PB_T_BQ, d, true);
+    put(PB_T_BK, d, false);
+    put(PB_T_BV, d, false);
+    put(PB_T_BO, d, true);
+    put(PB_T_B1, f, true);
+    put(PB_T_B2, d, true);
+    put(PB_T_LN1_G, d, true);
+    put(PB_T_LN1_B, d, true);
+    put(PB_T_LN2_G, d, true);
+    put(PB_T_LN2_B, d, true);
+    L.total = align_up(p, VEC_ALIGN);
+    return L;
+}
+
+struct GlobalsLayout {
+    size_t off[PB_G_COUNT];
+    size_t num[PB_G_COUNT];
+    size_t total;
+};
+
+GlobalsLayout globals_layout(const pb_config* c) {
+    const size_t d = c->d_model;
+    GlobalsLayout G{};
+    size_t p = 0;
+    auto put = [&](int t, size_t n) {
+        p = align_up(p, VEC_ALIGN);
+        G.off[t] = p;
+        G.num[t] = n;
+        p += n;
+    };
+    put(PB_G_EMBED, (size_t)c->vocab * d);
+    put(PB_G_POS, (size_t)c->max_pos * d);
+    put(PB_G_LNF_G, d);
+    put(PB_G_LNF_B, d);
+    G.total = align_up(p, VEC_ALIGN);
+    return G;
+}
+
+int popcount4(uint32_t m) { return (m & 1) + ((m >> 1) & 1) + ((m >> 2) & 1) + ((m >> 3) & 1); }
+
+size_t lora_layer_elems(const pb_config* c, int rank, uint32_t mask) {
+    return (size_t)popcount4(mask) * 2 * (size_t)rank * c->d_model;
+}
+
+// Everything the arena holds, in bytes.
+struct ArenaLayout {
+    int rs, kw;  // LoRA slot width (rank rounded up to 8) and packed width (multiple of 64)
+    size_t globals, layers, layer_bytes, loraA, loraB, loraA_layer, loraB_layer;
+    size_t x, u, qkv, attn, h, z, rowslot, tokens, slotscale, zf, logits, outtok, staging;
+    size_t staging_bytes, total;
+};
+
+ArenaLayout arena_layout(const pb_config* c) {
+    ArenaLayout a{};
+    const size_t d = c->d_model, f = c->d_ffn, L = c->n_layers, N = c->max_tokens;
+    const size_t B = c->max_batch, V = c->vocab;
+    a.rs = c->max_adapters > 0 ? (int)align_up(c->max_rank, 8) : 0;
+    a.kw = c->max_adapters > 0 ? (int)align_up((size_t)c->max_adapters * a.rs, 64) : 0;
+    a.layer_bytes = layer_layout(c).total * 2;
+    size_t p = 0;
+    auto take = [&](size_t bytes) {
+        p = align_up(p, ALIGN);
+        const size_t o = p;
+        p += bytes;
+        return o;
+    };
+    a.globals = take(globals_layout(c).total * 2);
+    a.layers = take(L * a.layer_bytes);
+    a.loraA_layer = 4 * (size_t)a.kw * d * 2;
+    a.loraB_layer = 4 * d * (size_t)a.kw * 2;
+    a.loraA = take(L * a.loraA_layer);
+    a.loraB = take(L * a.loraB_layer);
+    a.x = take(N * d * 4);
+    a.u = take(N * d * 2);
+    a.qkv = take(N * 3 * d * 2);
+    a.attn = take(N * d * 2);
+    a.h = take(N * f * 2);
+    a.z = take(N * 4 * (size_t)a.kw * 2);
+    a.rowslot = take(N * 4);
+    a.tokens = take(N * 4);
+    a.slotscale = take(MAX_SLOTS * 4);
+    a.zf = take(B * d * 4);
+    a.logits = take(B * V * 4);
+    a.outtok = take(B * 4);
+    a.staging_bytes = c->max_adapters > 0 ? L * lora_layer_elems(c, c->max_rank, 0xF) * 2 : 0;
+    a.staging = take(a.staging_bytes);
+    a.total = align_up(p, ALIGN);
+    return a;
+}
+
+bool is_pinned(const void* p, size_t bytes) {
+    if (!p) return false;
+    auto one = [](const void* q) {
+        hipPointerAttribute_t attr;
+        hipError_t e = hipPointerGetAttributes(&attr, q);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();  // clear the sticky error of the failed query
+            return false;
+        }
+        return attr.type == hipMemoryTypeHost;
+    };
+    if (!one(p)) return false;
+    if (bytes > 1 && !one((const char*)p + bytes - 1)) return false;
+    return true;
+}
+
+}  // namespace
+
+struct pb_model {
+    pb_config cfg;
+    ArenaLayout lay;
+    LayerLayout ll;
+    GlobalsLayout gl;
+    char* arena = nullptr;
+    hipStream_t copy = nullptr, compute = nullptr;
+    int device = 0;
+    std::vector<hipEvent_t> ev_layer;
+    hipEvent_t ev_globals = nullptr, ev_lora = nullptr, ev_load0 = nullptr, ev_load1 = nullptr;
+    bool streamed = false, lora_recorded = false;
+    double last_load_bytes = 0;
+    size_t chunk_bytes = 64u << 20;
+    int delay_us = 0;
+    // adapter slots
+    bool slot_valid[MAX_SLOTS] = {};
+    int slot_rank[MAX_SLOTS] = {};
+    uint32_t slot_mask[MAX_SLOTS] = {};
+    float slot_scale[MAX_SLOTS] = {};
+    // pinned host staging for the small per-call transfers
+    int32_t* h_tokens = nullptr;
+    int32_t* h_rowslot = nullptr;
+    float* h_scale = nullptr;
+    int32_t* h_outtok = nullptr;
+    float* h_logits = nullptr;
+    // per-kernel timing
+    bool timing = false;
+    std::vector<hipEvent_t> tev;
+    std::vector<int> tkind;
+    size_t tused = 0;
+    double ttotal[PB_K_COUNT] = {};
+    int64_t tcount[PB_K_COUNT] = {};
+
+    char* at(size_t off) { return arena + off; }
+    char* layer_ptr(int l) { return at(lay.layers + (size_t)l * lay.layer_bytes); }
+    char* ltensor(int l, int t) { return layer_ptr(l) + ll.off[t] * 2; }
+    char* gtensor(int t) { return at(lay.globals) + gl.off[t] * 2; }
+};
+
+extern "C" {
+
+const char* pb_last_error(void) { return g_err.c_str(); }
+
+size_t pb_layer_bytes(const pb_config* cfg) {
+    if (!config_ok(cfg, nullptr)) return 0;
+    return layer_layout(cfg).total * 2;
+}
+
+size_t pb_globals_bytes(const pb_config* cfg) {
+    if (!config_ok(cfg, nullptr)) return 0;
+    return globals_layout(cfg).total * 2;
+}
+
+int pb_layer_tensor(const pb_config* cfg, int32_t tensor, size_t* offset, size_t* numel) {
+    std::string why;
+    if (!config_ok(cfg, &why)) return fail(PB_EINVAL, "invalid config: %s", why.c_str());
+    if (tensor < 0 || tensor >= PB_T_COUNT) return fail(PB_EINVAL, "unknown layer tensor %d", tensor);
+    const LayerLayout L = layer_layout(cfg);
+    if (offset) *offset = L.off[tensor];
+    if (numel) *numel = L.num[tensor];
+    return PB_OK;
+}
+
+int pb_globals_tensor(const pb_config* cfg, int32_t tensor, size_t* offset, size_t* numel) {
+    std::string why;
+    if (!config_ok(cfg, &why)) return fail(PB_EINVAL, "invalid config: %s", why.c_str());
+    if (tensor < 0 || tensor >= PB_G_COUNT) return fail(PB_EINVAL, "unknown global tensor %d", tensor);
+    const GlobalsLayout G = globals_layout(cfg);
+    if (offset) *offset = G.off[tensor];
+    if (numel) *numel = G.num[tensor];
+    return PB_OK;
+}
+
+size_t pb_lora_layer_bytes(const pb_config* cfg, int32_t rank, uint32_t target_mask) {
+    if (!config_ok(cfg, nullptr) || rank < 1 || rank > cfg->max_rank || (target_mask & ~0xFu) ||
+        target_mask == 0)
+        return 0;
+    return lora_layer_elems(cfg, rank, target_mask) * 2;
+}
+
+int pb_lora_tensor(const pb_config* cfg, int32_t rank, uint32_t target_mask, int32_t target,
+                   int32_t which, size_t* offset, size_t* numel) {
+    if (pb_lora_layer_bytes(cfg, rank, target_mask) == 0)
+        return fail(PB_EINVAL, "invalid LoRA rank %d or target mask 0x%x", rank, target_mask);
+    if (target < 0 || target > 3 || !((target_mask >> target) & 1u))
+        return fail(PB_EINVAL, "target %d not in mask 0x%x", target, target_mask);
+    if (which != 0 && which != 1) return fail(PB_EINVAL, "which must be 0 (A) or 1 (B)");
+    int idx = 0;
+    for (int t = 0; t < target; ++t) idx += (target_mask >> t) & 1u;
+    const size_t rd = (size_t)rank * cfg->d_model;
+    if (offset) *offset = (size_t)idx * 2 * rd + (which ? rd : 0);
+    if (numel) *numel = rd;
+    return PB_OK;
+}
+
+size_t pb_arena_bytes(const pb_config* cfg) {
+    if (!config_ok(cfg, nullptr)) return 0;
+    return arena_layout(cfg).total;
+}
+
+int pb_host_alloc(size_t bytes, void** out) {
+    if (!out || bytes == 0) return fail(PB_EINVAL, "pb_host_alloc: bad arguments");
+    *out = nullptr;
+    hipError_t e = hipHostMalloc(out, bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        *out = nullptr;
+        return fail(PB_ENOMEM, "hipHostMalloc(%zu) failed: %s", bytes, hipGetErrorString(e));
+    }
+    return PB_OK;
+}
+
+int pb_host_free(void* ptr) {
+    if (!ptr) return PB_OK;
+    HIP_TRY(hipHostFree(ptr));
+    return PB_OK;
+}
+
+int pb_model_create(const pb_config* cfg, void* dev_arena, size_t arena_bytes, void* copy_stream,
+                    void* compute_stream, pb_model** out) {
+    if (!out) return fail(PB_EINVAL, "out is NULL");
+    *out = nullptr;
+    std::string why;
+    if (!config_ok(cfg, &why)) return fail(PB_EINVAL, "invalid config: %s", why.c_str());
+    if (!dev_arena || ((uintptr_t)dev_arena % ALIGN))
+        return fail(PB_EINVAL, "device arena must be non-NULL and 256-byte aligned");
+    if (copy_stream == compute_stream)
+        return fail(PB_EINVAL, "copy and compute streams must differ");
+    const ArenaLayout lay = arena_layout(cfg);
+    if (arena_bytes < lay.total)
+        return fail(PB_ENOMEM, "arena of %zu bytes is smaller than the %zu required", arena_bytes,
+                    lay.total);
+    pb_model* m = new pb_model();
+    m->cfg = *cfg;
+    m->lay = lay;
+    m->ll = layer_layout(cfg);
+    m->gl = globals_layout(cfg);
+    m->arena = (char*)dev_arena;
+    m->copy = (hipStream_t)copy_stream;
+    m->compute = (hipStream_t)compute_stream;
+    auto cleanup = [&](int code) {
+        pb_destroy(m);
+        return code;
+    };
+    if (hipGetDevice(&m->device) != hipSuccess) return cleanup(fail(PB_EHIP, "hipGetDevice failed"));
+    m->ev_layer.assign(cfg->n_layers, nullptr);
+    for (auto& e : m->ev_layer)
+        if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess)
+            return cleanup(fail(PB_EHIP, "hipEventCreate failed"));
+    if (hipEventCreateWithFlags(&m->ev_globals, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&m->ev_lora, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreate(&m->ev_load0) != hipSuccess || hipEventCreate(&m->ev_load1) != hipSuccess)
+        return cleanup(fail(PB_EHIP, "hipEventCreate failed"));
+    const size_t B = cfg->max_batch, N = cfg->max_tokens, V = cfg->vocab;
+    if (hipHostMalloc((void**)&m->h_tokens, N * 4, 0) != hipSuccess ||
+        hipHostMalloc((void**)&m->h_rowslot, N * 4, 0) != hipSuccess ||
+        hipHostMalloc((void**)&m->h_scale, MAX_SLOTS * 4, 0) != hipSuccess ||
+        hipHostMalloc((void**)&m->h_outtok, B * 4, 0) != hipSuccess ||
+        hipHostMalloc((void**)&m->h_logits, B * V * 4, 0) != hipSuccess)
+        return cleanup(fail(PB_ENOMEM, "pinned staging allocation failed"));
+    // LoRA slots start as zeros: an empty slot contributes exactly nothing
+    {
+        const size_t end = lay.loraB + (size_t)cfg->n_layers * lay.loraB_layer;
+        if (end > lay.loraA && hipMemsetAsync(m->at(lay.loraA), 0, end - lay.loraA, m->copy) != hipSuccess)
+            return cleanup(fail(PB_EHIP, "hipMemsetAsync of the LoRA slots failed"));
+    }
+    if (hipStreamSynchronize(m->copy) != hipSuccess)
+        return cleanup(fail(PB_EHIP, "hipStreamSynchronize failed"));
+    *out = m;
+    return PB_OK;
+}
+
+int pb_destroy(pb_model* m) {
+    if (!m) return PB_OK;
+    if (m->copy) (void)hipStreamSynchronize(m->copy);
+    if (m->compute) (void)hipStreamSynchronize(m->compute);
+    for (auto e : m->ev_layer)
+        if (e) (void)hipEventDestroy(e);
+    for (auto e : m->tev)
+        if (e) (void)hipEventDestroy(e);
+    for (auto e : {m->ev_globals, m->ev_lora, m->ev_load0, m->ev_load1})
+        if (e) (void)hipEventDestroy(e);
+    for (void* p : {(void*)m->h_tokens, (void*)m->h_rowslot, (void*)m->h_scale, (void*)m->h_outtok,
+                    (void*)m->h_logits})
+        if (p) (void)hipHostFree(p);
+    delete m;
+    return PB_OK;
+}
+
+int pb_set_chunk_bytes(pb_model* m, size_t bytes) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    if (bytes < (1u << 20)) return fail(PB_EINVAL, "chunk must be at least 1 MiB");
+    m->chunk_bytes = bytes;
+    return PB_OK;
+}
+
+int pb_set_stream_delay_us(pb_model* m, int32_t us) {
+    if (!m || us < 0) return fail(PB_EINVAL, "bad arguments");
+    m->delay_us = us;
+    return PB_OK;
+}
+
+static int copy_chunked(pb_model* m, char* dst, const char* src, size_t bytes) {
+    for (size_t o = 0; o < bytes; o += m->chunk_bytes) {
+        const size_t n = std::min(m->chunk_bytes, bytes - o);
+        HIP_TRY(hipMemcpyAsync(dst + o, src + o, n, hipMemcpyHostToDevice, m->copy));
+    }
+    return PB_OK;
+}
+
+int pb_stream_layers(pb_model* m, const int32_t* layer_order, int32_t n_layers,
+                     const void* const* host_layers, const void* host_globals) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    const int L = m->cfg.n_layers;
+    if (n_layers != L) return fail(PB_EINVAL, "layer_order has %d entries, the model %d layers", n_layers, L);
+    if (!layer_order || !host_layers || !host_globals) return fail(PB_EINVAL, "NULL argument");
+    std::vector<char> seen(L, 0);
+    for (int i = 0; i < L; ++i) {
+        const int l = layer_order[i];
+        if (l < 0 || l >= L || seen[l]) return fail(PB_EINVAL, "layer_order is not a permutation of 0..%d", L - 1);
+        seen[l] = 1;
+    }
+    const size_t lb = m->lay.layer_bytes, gb = m->gl.total * 2;
+    if (!is_pinned(host_globals, gb)) return fail(PB_ENOTPINNED, "globals blob is not pinned host memory");
+    for (int l = 0; l < L; ++l)
+        if (!is_pinned(host_layers[l], lb)) return fail(PB_ENOTPINNED, "layer %d blob is not pinned host memory", l);
+    HIP_TRY(hipEventRecord(m->ev_load0, m->copy));
+    int rc = copy_chunked(m, m->at(m->lay.globals), (const char*)host_globals, gb);
+    if (rc) return rc;
+    HIP_TRY(hipEventRecord(m->ev_globals, m->copy));
+    for (int i = 0; i < L; ++i) {
+        const int l = layer_order[i];
+        if (m->delay_us > 0 && i > 0) std::this_thread::sleep_for(std::chrono::microseconds(m->delay_us));
+        rc = copy_chunked(m, m->layer_ptr(l), (const char*)host_layers[l], lb);
+        if (rc) return rc;
+        HIP_TRY(hipEventRecord(m->ev_layer[l], m->copy));
+    }
+    HIP_TRY(hipEventRecord(m->ev_load1, m->copy));
+    m->last_load_bytes = (double)gb + (double)L * (double)lb;
+    m->streamed = true;
+    return PB_OK;
+}
+
+int pb_attach_lora(pb_model* m, int32_t slot, int32_t rank, float alpha, uint32_t target_mask,
+                   const void* const* host_lora) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    const pb_config& c = m->cfg;
+    if (slot < 0 || slot >= c.max_adapters) return fail(PB_EINVAL, "slot %d outside [0, %d)", slot, c.max_adapters);
+    if (rank < 1 || rank > c.max_rank) return fail(PB_EINVAL, "rank %d outside [1, %d]", rank, c.max_rank);
+    if (target_mask == 0 || (target_mask & ~0xFu)) return fail(PB_EINVAL, "bad target mask 0x%x", target_mask);
+    if (!std::isfinite(alpha)) return fail(PB_EINVAL, "alpha must be finite");
+    if (!host_lora) return fail(PB_EINVAL, "host_lora is NULL");
+    const size_t elems = lora_layer_elems(&c, rank, target_mask);
+    const size_t bytes = elems * 2;
+    for (int l = 0; l < c.n_layers; ++l)
+        if (!is_pinned(host_lora[l], bytes)) return fail(PB_ENOTPINNED, "LoRA blob of layer %d is not pinned", l);
+    char* stage = m->at(m->lay.staging);
+    for (int l = 0; l < c.n_layers; ++l)
+        HIP_TRY(hipMemcpyAsync(stage + (size_t)l * bytes, host_lora[l], bytes, hipMemcpyHostToDevice, m->copy));
+    HIP_TRY(pb::launch_lora_pack(c.dtype, stage, elems, c.n_layers, c.d_model, rank, target_mask, slot,
+                                 m->lay.rs, m->lay.kw, m->at(m->lay.loraA), m->at(m->lay.loraB),
+                                 m->copy));
+    HIP_TRY(hipEventRecord(m->ev_lora, m->copy));
+    m->lora_recorded = true;
+    m->slot_valid[slot] = true;
+    m->slot_rank[slot] = rank;
+    m->slot_mask[slot] = target_mask;
+    m->slot_scale[slot] = alpha / (float)rank;
+    return PB_OK;
+}
+
+int pb_poison_weights(pb_model* m, int32_t value) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    const ArenaLayout& a = m->lay;
+    HIP_TRY(hipMemsetAsync(m->at(a.globals), value & 0xFF, a.loraA - a.globals, m->copy));
+    // LoRA slots go back to zeros (a NaN in an unused slot would reach every
+    // output through the zero columns of the packed expand); they hold no
+    // adapter until the next pb_attach_lora
+    const size_t end = a.loraB + (size_t)m->cfg.n_layers * a.loraB_layer;
+    if (end > a.loraA) HIP_TRY(hipMemsetAsync(m->at(a.loraA), 0, end - a.loraA, m->copy));
+    for (int s = 0; s < MAX_SLOTS; ++s) m->slot_valid[s] = false;
+    m->streamed = false;
+    return PB_OK;
+}
+
+int pb_last_load_stats(pb_model* m, double* bytes, double* ms) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    if (!m->streamed) return fail(PB_ESTATE, "no completed pb_stream_layers");
+    float t = 0.f;
+    HIP_TRY(hipEventSynchronize(m->ev_load1));
+    HIP_TRY(hipEventElapsedTime(&t, m->ev_load0, m->ev_load1));
+    if (bytes) *bytes = m->last_load_bytes;
+    if (ms) *ms = t;
+    return PB_OK;
+}
+
+int pb_set_kernel_timing(pb_model* m, int32_t enable) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    m->timing = enable != 0;
+    return PB_OK;
+}
+
+int pb_get_kernel_timing(pb_model* m, int32_t kind, double* total_ms, int64_t* launches) {
+    if (!m || kind < 0 || kind >= PB_K_COUNT) return fail(PB_EINVAL, "bad arguments");
+    if (total_ms) *total_ms = m->ttotal[kind];
+    if (launches) *launches = m->tcount[kind];
+    return PB_OK;
+}
+
+int pb_reset_kernel_timing(pb_model* m) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    for (int k = 0; k < PB_K_COUNT; ++k) {
+        m->ttotal[k] = 0;
+        m->tcount[k] = 0;
+    }
+    return PB_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Brackets one kernel launch with timing events when timing is enabled.
+struct Timed {
+    pb_model* m;
+    int kind;
+    size_t idx;
+    Timed(pb_model* mm, int k) : m(mm), kind(k), idx(0) {
+        if (!m->timing) return;
+        if (m->tused + 2 > m->tev.size()) {
+            hipEvent_t a, b;
+            (void)hipEventCreate(&a);
+            (void)hipEventCreate(&b);
+            m->tev.push_back(a);
+            m->tev.push_back(b);
+            m->tkind.push_back(-1);
+        }
+        idx = m->tused;
+        m->tused += 2;
+        m->tkind[idx / 2] = kind;
+        (void)hipEventRecord(m->tev[idx], m->compute);
+    }
+    ~Timed() {
+        if (m->timing) (void)hipEventRecord(m->tev[idx + 1], m->compute);
+    }
+};
+
+int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_union) {
+    const pb_config& c = m->cfg;
+    const ArenaLayout& a = m->lay;
+    const int dt = c.dtype;
+    const int d = c.d_model, F = c.d_ffn, H = c.n_heads, hd = d / H, L = c.n_layers;
+    const int N = B * T;
+    hipStream_t s = m->compute;
+    float* x = (float*)m->at(a.x);
+    char* u = m->at(a.u);
+    char* qkv = m->at(a.qkv);
+    char* attn = m->at(a.attn);
+    char* hbuf = m->at(a.h);
+    char* z = m->at(a.z);
+    const int kw = a.kw;
+    const int32_t* rowslot = (const int32_t*)m->at(a.rowslot);
+    const float* sscale = (const float*)m->at(a.slotscale);
+
+    HIP_TRY(hipStreamWaitEvent(s, m->ev_globals, 0));
+    if (use_lora) HIP_TRY(hipStreamWaitEvent(s, m->ev_lora, 0));
+    {
+        Timed t(m, PB_K_EMBED);
+        HIP_TRY(pb::launch_embed(dt, (const int32_t*)m->at(a.tokens), m->gtensor(PB_G_EMBED),
+                                 m->gtensor(PB_G_POS), x, N, T, d, s));
+    }
+    const bool qkv_lora = use_lora && (lora_union & (PB_LORA_Q | PB_LORA_K | PB_LORA_V));
+    const bool o_lora = use_lora && (lora_union & PB_LORA_O);
+    for (int l = 0; l < L; ++l) {
+        HIP_TRY(hipStreamWaitEvent(s, m->ev_layer[l], 0));
+        char* Aq = m->at(a.loraA) + (size_t)l * a.loraA_layer;  // [4][kw][d]
+        char* Bq = m->at(a.loraB) + (size_t)l * a.loraB_layer;  // [4][d][kw]
+        {
+            Timed t(m, PB_K_LN);
+            HIP_TRY(pb::launch_layernorm(dt, x, 1, 0, m->ltensor(l, PB_T_LN1_G), m->ltensor(l, PB_T_LN1_B),
+                                         u, false, N, d, c.ln_eps, s));
+        }
+        if (qkv_lora) {
+            Timed t(m, PB_K_LORA_SHRINK);
+            pb::GemmParams p{};
+            p.X = u; p.ldx = d; p.W = Aq; p.ldw = d; p.M = N; p.N = 3 * kw; p.K1 = d;
+            p.C = z; p.ldc = 4 * kw;
+            p.row_slot = rowslot; p.slot_scale = sscale; p.slot_width = a.rs; p.kw = kw;
+            HIP_TRY(pb::launch_gemm(dt, 4, pb::EPI_SHRINK, p, s));
+        }
+        {
+            Timed t(m, PB_K_GEMM_QKV);
+            pb::GemmParams p{};
+            p.X = u; p.ldx = d; p.W = m->ltensor(l, PB_T_WQ); p.ldw = d; p.M = N; p.N = 3 * d; p.K1 = d;
+            if (qkv_lora) {
+                p.X2 = z; p.ldx2 = 4 * kw; p.W2 = Bq; p.ldw2 = kw; p.K2 = kw; p.group = d;
+                p.k2_mask = lora_union & 7u; p.x2_group_stride = kw;
+            }
+            p.bias = m->ltensor(l, PB_T_BQ);
+            p.C = qkv; p.ldc = 3 * d;
+            p.qscale = 1.0f / std::sqrt((float)hd); p.qcols = d;
+            HIP_TRY(pb::launch_gemm(dt, 0, pb::EPI_QKV, p, s));
+        }
+        {
+            Timed t(m, PB_K_ATTN);
+            HIP_TRY(pb::launch_attention(dt, qkv, attn, B, T, H, hd, s));
+        }
+        if (o_lora) {
+            Timed t(m, PB_K_LORA_SHRINK);
+            pb::GemmParams p{};
+            p.X = attn; p.ldx = d; p.W = Aq + 3 * (size_t)kw * d * 2; p.ldw = d; p.M = N; p.N = kw; p.K1 = d;
+            p.C = z + 3 * (size_t)kw * 2; p.ldc = 4 * kw;
+            p.row_slot = rowslot; p.slot_scale = sscale; p.slot_width = a.rs; p.kw = kw;
+            HIP_TRY(pb::launch_gemm(dt, 4, pb::EPI_SHRINK, p, s));
+        }
+        {
+            Timed t(m, PB_K_GEMM_O);
+            pb::GemmParams p{};
+            p.X = attn; p.ldx = d; p.W = m->ltensor(l, PB_T_WO); p.ldw = d; p.M = N; p.N = d; p.K1 = d;
+            if (o_lora) {
+                p.X2 = z + 3 * (size_t)kw * 2; p.ldx2 = 4 * kw; p.W2 = Bq + 3 * (size_t)d * kw * 2;
+                p.ldw2 = kw; p.K2 = kw; p.group = d; p.k2_mask = 1u; p.x2_group_stride = 0;
+            }
+            p.bias = m->ltensor(l, PB_T_BO);
+            p.R = x; p.ldr = d;
+            HIP_TRY(pb::launch_gemm(dt, 1, pb::EPI_RESID, p, s));
+        }
+        {
+            Timed t(m, PB_K_LN);
+            HIP_TRY(pb::launch_layernorm(dt, x, 1, 0, m->ltensor(l, PB_T_LN2_G), m->ltensor(l, PB_T_LN2_B),
+                                         u, false, N, d, c.ln_eps, s));
+        }
+        {
+            Timed t(m, PB_K_GEMM_FC1);
+            pb::GemmParams p{};
+            p.X = u; p.ldx = d; p.W = m->ltensor(l, PB_T_W1); p.ldw = d; p.M = N; p.N = F; p.K1 = d;
+            p.bias = m->ltensor(l, PB_T_B1);
+            p.C = hbuf; p.ldc = F;
+            HIP_TRY(pb::launch_gemm(dt, 2, pb::EPI_RELU, p, s));
+        }
+        {
+            Timed t(m, PB_K_GEMM_FC2);
+            pb::GemmParams p{};
+            p.X = hbuf; p.ldx = F; p.W = m->ltensor(l, PB_T_W2); p.ldw = F; p.M = N; p.N = d; p.K1 = F;
+            p.bias = m->ltensor(l, PB_T_B2);
+            p.R = x; p.ldr = d;
+            HIP_TRY(pb::launch_gemm(dt, 3, pb::EPI_RESID, p, s));
+        }
+    }
+    float* zf = (float*)m->at(a.zf);
+    {
+        Timed t(m, PB_K_LN);
+        HIP_TRY(pb::launch_layernorm(dt, x, T, T - 1, m->gtensor(PB_G_LNF_G), m->gtensor(PB_G_LNF_B), zf,
+                                     true, B, d, c.ln_eps, s));
+    }
+    {
+        Timed t(m, PB_K_LM_HEAD);
+        HIP_TRY(pb::launch_lm_head(dt, zf, B, m->gtensor(PB_G_EMBED), c.vocab, d,
+                                   (float*)m->at(a.logits), s));
+    }
+    {
+        Timed t(m, PB_K_ARGMAX);
+        HIP_TRY(pb::launch_argmax((const float*)m->at(a.logits), B, c.vocab, (int32_t*)m->at(a.outtok), s));
+    }
+    return PB_OK;
+}
+
+}  // namespace
+
+extern "C" int pb_prefill_first_token(pb_model* m, const int32_t* tokens, int32_t B, int32_t T,
+                                      const int32_t* adapter_of_seq, int32_t* out_tokens,
+                                      float* out_logits) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    const pb_config& c = m->cfg;
+    if (!tokens || !out_tokens) return fail(PB_EINVAL, "tokens and out_tokens must be non-NULL");
+    if (B < 1 || B > c.max_batch) return fail(PB_EINVAL, "B=%d outside [1, %d]", B, c.max_batch);
+    if (T < 1 || T > c.max_pos) return fail(PB_EINVAL, "T=%d outside [1, %d]", T, c.max_pos);
+    if ((int64_t)B * T > c.max_tokens) return fail(PB_EINVAL, "B*T=%lld exceeds max_tokens=%d", (long long)B * T, c.max_tokens);
+    if (!m->streamed) return fail(PB_ESTATE, "prefill before pb_stream_layers");
+    const int N = B * T;
+    for (int i = 0; i < N; ++i)
+        if (tokens[i] < 0 || tokens[i] >= c.vocab) return fail(PB_EINVAL, "token %d at %d outside [0, %d)", tokens[i], i, c.vocab);
+    bool use_lora = false;
+    uint32_t lora_union = 0;
+    for (int b = 0; b < B; ++b) {
+        const int a = adapter_of_seq ? adapter_of_seq[b] : -1;
+        if (a < -1 || a >= c.max_adapters) return fail(PB_EINVAL, "adapter %d of sequence %d outside [-1, %d)", a, b, c.max_adapters);
+        if (a >= 0) {
+            if (!m->slot_valid[a]) return fail(PB_ESTATE, "adapter slot %d holds no adapter", a);
+            use_lora = true;
+            lora_union |= m->slot_mask[a];
+        }
+        for (int t = 0; t < T; ++t) m->h_rowslot[b * T + t] = a;
+    }
+    std::memcpy(m->h_tokens, tokens, (size_t)N * 4);
+    for (int s = 0; s < MAX_SLOTS; ++s) m->h_scale[s] = m->slot_valid[s] ? m->slot_scale[s] : 0.f;
+    const ArenaLayout& a = m->lay;
+    hipStream_t s = m->compute;
+    m->tused = 0;
+    HIP_TRY(hipMemcpyAsync(m->at(a.tokens), m->h_tokens, (size_t)N * 4, hipMemcpyHostToDevice, s));
+    HIP_TRY(hipMemcpyAsync(m->at(a.rowslot), m->h_rowslot, (size_t)N * 4, hipMemcpyHostToDevice, s));
+    HIP_TRY(hipMemcpyAsync(m->at(a.slotscale), m->h_scale, MAX_SLOTS * 4, hipMemcpyHostToDevice, s));
+    int rc = enqueue_forward(m, B, T, use_lora, lora_union);
+    if (rc) {
+        (void)hipStreamSynchronize(s);
+        return rc;
+    }
+    HIP_TRY(hipMemcpyAsync(m->h_outtok, m->at(a.outtok), (size_t)B * 4, hipMemcpyDeviceToHost, s));
+    if (out_logits)
+        HIP_TRY(hipMemcpyAsync(m->h_logits, m->at(a.logits), (size_t)B * c.vocab * 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    std::memcpy(out_tokens, m->h_outtok, (size_t)B * 4);
+    if (out_logits) std::memcpy(out_logits, m->h_logits, (size_t)B * c.vocab * 4);
+    if (m->timing) {
+        for (size_t i = 0; i + 1 < m->tused; i += 2) {
+            float ms = 0.f;
+            HIP_TRY(hipEventElapsedTime(&ms, m->tev[i], m->tev[i + 1]));
+            const int k = m->tkind[i / 2];
+            m->ttotal[k] += ms;
+            m->tcount[k] += 1;
+        }
+    }
+    return PB_OK;
+}

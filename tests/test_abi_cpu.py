@@ -1,0 +1,85 @@
+"""C ABI checks that need no GPU: the library loads, exports every function
+the public headers declare, and answers layout queries."""
+import ctypes
+import glob
+import os
+import re
+
+import pytest
+
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        for m in re.finditer(r"\b(pb_[a-z0-9_]+)\s*\(", text):
+            names.add(m.group(1))
+    return sorted(names)
+
+
+def test_headers_declare_the_boundary():
+    names = _declared()
+    for required in ("pb_model_create", "pb_stream_layers", "pb_attach_lora",
+                     "pb_prefill_first_token", "pb_destroy", "pb_last_error"):
+        assert required in names
+
+
+@pytest.mark.parametrize("name", _declared())
+def test_library_exports_declared_symbol(name):
+    from paper_2503_17707_amd import binding as pb
+
+    assert hasattr(pb.lib(), name)
+
+
+def test_layout_queries():
+    from paper_2503_17707_amd import binding as pb
+
+    w = synth.WORKLOADS["opt-1.3b"]
+    cfg = pb.make_config(w)
+    L = pb.lib()
+    lb = L.pb_layer_bytes(ctypes.byref(cfg))
+    d, f = w.d_model, w.d_ffn
+    assert lb >= 2 * w.layer_params()
+    assert lb - 2 * w.layer_params() < 4096  # only alignment padding
+    off_q, n_q = pb.layer_tensor(cfg, "wq")
+    off_k, _ = pb.layer_tensor(cfg, "wk")
+    off_v, _ = pb.layer_tensor(cfg, "wv")
+    assert n_q == d * d and off_k == off_q + d * d and off_v == off_k + d * d
+    off_bq, _ = pb.layer_tensor(cfg, "bq")
+    off_bk, _ = pb.layer_tensor(cfg, "bk")
+    assert off_bk == off_bq + d
+    # tensors do not overlap and fit the blob
+    spans = sorted(pb.layer_tensor(cfg, n) for n in synth.LAYER_TENSORS)
+    for (o1, n1), (o2, _) in zip(spans, spans[1:]):
+        assert o1 + n1 <= o2
+    assert spans[-1][0] + spans[-1][1] <= lb // 2
+    gb = L.pb_globals_bytes(ctypes.byref(cfg))
+    assert gb >= 2 * w.global_params()
+    # LoRA blob: A [r, d] then B [d, r] per target, q before v
+    mask = 1 | 4
+    assert L.pb_lora_layer_bytes(ctypes.byref(cfg), 16, mask) == 2 * 2 * 2 * 16 * d
+    assert pb.lora_tensor(cfg, 16, mask, "q", "A") == (0, 16 * d)
+    assert pb.lora_tensor(cfg, 16, mask, "q", "B") == (16 * d, 16 * d)
+    assert pb.lora_tensor(cfg, 16, mask, "v", "A") == (32 * d, 16 * d)
+    assert L.pb_arena_bytes(ctypes.byref(cfg)) > w.storage_bytes()
+    del f
+
+
+def test_invalid_configs_are_refused():
+    from paper_2503_17707_amd import binding as pb
+
+    L = pb.lib()
+    base = pb.make_config(synth.WORKLOADS["tiny"])
+    for field, value in (("d_model", 200), ("n_heads", 3), ("d_ffn", 100), ("n_layers", 0),
+                         ("dtype", 7), ("max_rank", 0), ("max_adapters", 17)):
+        cfg = pb.Config.from_buffer_copy(base)
+        setattr(cfg, field, value)
+        assert L.pb_arena_bytes(ctypes.byref(cfg)) == 0, field
+        off = ctypes.c_size_t()
+        assert L.pb_layer_tensor(ctypes.byref(cfg), 0, ctypes.byref(off), None) == pb.PB_EINVAL
+        assert L.pb_last_error().decode()
