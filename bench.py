@@ -51,6 +51,39 @@ def kernel_flops(w, kind):
     return None
 
 
+def source_sha256():
+    import glob
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2503_17707_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def profiled_traffic(workload, kind):
+    """HBM bytes per launch of a kernel kind from the committed rocprofv3 counter
+    summary, or None when absent or taken from other kernel sources."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_%s.md" % workload)
+    if not os.path.exists(path):
+        return None
+    block, inside = {}, False
+    for line in open(path):
+        line = line.strip()
+        if line.startswith("```traffic"):
+            inside = True
+            continue
+        if inside and line.startswith("```"):
+            break
+        if inside and line:
+            k, v = line.split()
+            block[k] = v
+    if block.get("source_sha256") != source_sha256() or kind not in block:
+        return None
+    return float(block[kind])
+
+
 def oracle_baseline(w, n_layers):
     """Time the CPU oracle on the first n_layers of the workload (plus the LM head)."""
     import numpy as np
@@ -108,6 +141,9 @@ def main():
     ap.add_argument("--cold-reps", type=int, default=5)
     ap.add_argument("--oracle-layers", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="only run a plain device copy of this many MiB (3 times) and exit: "
+                         "the reference kernel for scaling HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -117,6 +153,16 @@ def main():
 
     import numpy as np
     import torch
+
+    if args.calibrate_copy_mib:
+        n = args.calibrate_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration_copy_bytes": n, "copies": 3}), flush=True)
+        return
 
     import synth
     from paper_2503_17707_amd import binding as pb
@@ -206,7 +252,8 @@ def main():
     avg_ms = kt[dom][0] / kt[dom][1]
     achieved = kernel_flops(w, dom) / (avg_ms / 1e3) / 1e12
     roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": MFMA_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": achieved / MFMA_PEAK_TFLOPS, "traffic": None,
+                "unit": "TFLOP/s", "frac": achieved / MFMA_PEAK_TFLOPS,
+                "traffic": profiled_traffic(w.name, dom), "traffic_unit": "bytes per launch",
                 "avg_launch_ms": avg_ms, "flops_per_launch": kernel_flops(w, dom)}
     m.destroy()
     hw.free()

@@ -13,7 +13,8 @@ from typing import Dict, List, Optional, Sequence
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "lib", "libpipeboost.so")
+# PIPEBOOST_LIB selects another build of the same library (e.g. a tuning variant)
+LIB_PATH = os.environ.get("PIPEBOOST_LIB") or os.path.join(HERE, "lib", "libpipeboost.so")
 
 PB_OK, PB_EINVAL, PB_ENOTPINNED, PB_ENOMEM, PB_EHIP, PB_ESTATE = 0, -1, -2, -3, -4, -5
 PB_BF16, PB_F16 = 0, 1

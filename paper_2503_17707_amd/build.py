@@ -5,6 +5,7 @@ Every HIP source is compiled with packed FP32 instructions disabled
 warns that it does not know the feature, which is harmless.
 """
 import concurrent.futures as cf
+import hashlib
 import os
 import subprocess
 import sys
@@ -21,10 +22,11 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH, "-Wall", "-Wno-
          "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]
 
 
-def _compile(src: str, obj_dir: str) -> str:
+def _compile(src: str, obj_dir: str, defines=()) -> str:
     obj = os.path.join(obj_dir, os.path.splitext(src)[0] + ".o")
     lang = ["-x", "hip"] if src.endswith(".cpp") else []
-    cmd = ["hipcc", "-c"] + lang + [os.path.join(CSRC, src), "-o", obj] + FLAGS
+    cmd = (["hipcc", "-c"] + lang + [os.path.join(CSRC, src), "-o", obj] + FLAGS
+           + ["-D" + d for d in defines])
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("compile of %s failed:\n%s\n%s" % (src, " ".join(cmd), r.stderr))
@@ -34,21 +36,23 @@ def _compile(src: str, obj_dir: str) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    obj_dir = os.path.join(ROOT, "_build", "pipeboost")
+def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
+    """Compile and link; `out` and `defines` (NAME=VALUE) select a variant build."""
+    tag = hashlib.md5(repr((out, tuple(defines))).encode()).hexdigest()[:10]
+    obj_dir = os.path.join(ROOT, "_build", "pipeboost_" + tag)
     os.makedirs(obj_dir, exist_ok=True)
-    os.makedirs(OUT_DIR, exist_ok=True)
+    os.makedirs(os.path.dirname(out), exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, obj_dir), SOURCES))
-    tmp = LIB + ".tmp%d" % os.getpid()
+        objs = list(ex.map(lambda s: _compile(s, obj_dir, defines), SOURCES))
+    tmp = out + ".tmp%d" % os.getpid()
     cmd = ["hipcc", "-shared", "-fPIC", "--offload-arch=" + ARCH, "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n%s\n%s" % (" ".join(cmd), r.stderr))
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
     if verbose:
-        print("built", LIB)
-    return LIB
+        print("built", out)
+    return out
 
 
 if __name__ == "__main__":

@@ -34,9 +34,18 @@ struct GemmParams {
     const int32_t* row_slot; const float* slot_scale; int slot_width; int kw;
 };
 
+// Device scratch for split-K partials (fp32 [splits][M][N]); splitting is
+// skipped when it is absent or too small.
+struct GemmWorkspace {
+    void* ws;
+    size_t bytes;
+};
+
 // role: 0 qkv, 1 o, 2 fc1, 3 fc2, 4 shrink (selects the instantiation; each
-// role has its own kernel symbol so profiles separate them).
-hipError_t launch_gemm(int dtype, int role, int epi, const GemmParams& p, hipStream_t s);
+// role has its own kernel symbol so profiles separate them).  Requires every
+// operand offset (rows * leading dimension) to fit in 31 bits.
+hipError_t launch_gemm(int dtype, int role, int epi, const GemmParams& p, const GemmWorkspace& ws,
+                       hipStream_t s);
 
 // Causal multi-head self-attention over a batch of equal-length sequences.
 // qkv: [B*T, 3d] (q already divided by sqrt(head_dim)); out: [B*T, d].

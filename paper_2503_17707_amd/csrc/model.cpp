@@ -51,6 +51,7 @@ constexpr size_t ALIGN = 256;
 constexpr int MAX_SLOTS = 16;
 constexpr int MAX_RANK = 64;
 constexpr size_t VEC_ALIGN = 128;  // elements (256 bytes of dt)
+constexpr size_t GEMM_WS_BYTES = 64u << 20;  // split-K partials
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -148,7 +149,7 @@ size_t lora_layer_elems(const pb_config* c, int rank, uint32_t mask) {
 struct ArenaLayout {
     int rs, kw;  // LoRA slot width (rank rounded up to 8) and packed width (multiple of 64)
     size_t globals, layers, layer_bytes, loraA, loraB, loraA_layer, loraB_layer;
-    size_t x, u, qkv, attn, h, z, rowslot, tokens, slotscale, zf, logits, outtok, staging;
+    size_t x, u, qkv, attn, h, z, rowslot, tokens, slotscale, zf, logits, outtok, staging, ws;
     size_t staging_bytes, total;
 };
 
@@ -186,6 +187,7 @@ ArenaLayout arena_layout(const pb_config* c) {
     a.outtok = take(B * 4);
     a.staging_bytes = c->max_adapters > 0 ? L * lora_layer_elems(c, c->max_rank, 0xF) * 2 : 0;
     a.staging = take(a.staging_bytes);
+    a.ws = take(GEMM_WS_BYTES);
     a.total = align_up(p, ALIGN);
     return a;
 }
@@ -570,6 +572,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
     const int kw = a.kw;
     const int32_t* rowslot = (const int32_t*)m->at(a.rowslot);
     const float* sscale = (const float*)m->at(a.slotscale);
+    const pb::GemmWorkspace gws{m->at(a.ws), GEMM_WS_BYTES};
 
     HIP_TRY(hipStreamWaitEvent(s, m->ev_globals, 0));
     if (use_lora) HIP_TRY(hipStreamWaitEvent(s, m->ev_lora, 0));
@@ -595,7 +598,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             p.X = u; p.ldx = d; p.W = Aq; p.ldw = d; p.M = N; p.N = 3 * kw; p.K1 = d;
             p.C = z; p.ldc = 4 * kw;
             p.row_slot = rowslot; p.slot_scale = sscale; p.slot_width = a.rs; p.kw = kw;
-            HIP_TRY(pb::launch_gemm(dt, 4, pb::EPI_SHRINK, p, s));
+            HIP_TRY(pb::launch_gemm(dt, 4, pb::EPI_SHRINK, p, gws, s));
         }
         {
             Timed t(m, PB_K_GEMM_QKV);
@@ -608,7 +611,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             p.bias = m->ltensor(l, PB_T_BQ);
             p.C = qkv; p.ldc = 3 * d;
             p.qscale = 1.0f / std::sqrt((float)hd); p.qcols = d;
-            HIP_TRY(pb::launch_gemm(dt, 0, pb::EPI_QKV, p, s));
+            HIP_TRY(pb::launch_gemm(dt, 0, pb::EPI_QKV, p, gws, s));
         }
         {
             Timed t(m, PB_K_ATTN);
@@ -620,7 +623,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             p.X = attn; p.ldx = d; p.W = Aq + 3 * (size_t)kw * d * 2; p.ldw = d; p.M = N; p.N = kw; p.K1 = d;
             p.C = z + 3 * (size_t)kw * 2; p.ldc = 4 * kw;
             p.row_slot = rowslot; p.slot_scale = sscale; p.slot_width = a.rs; p.kw = kw;
-            HIP_TRY(pb::launch_gemm(dt, 4, pb::EPI_SHRINK, p, s));
+            HIP_TRY(pb::launch_gemm(dt, 4, pb::EPI_SHRINK, p, gws, s));
         }
         {
             Timed t(m, PB_K_GEMM_O);
@@ -632,7 +635,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             }
             p.bias = m->ltensor(l, PB_T_BO);
             p.R = x; p.ldr = d;
-            HIP_TRY(pb::launch_gemm(dt, 1, pb::EPI_RESID, p, s));
+            HIP_TRY(pb::launch_gemm(dt, 1, pb::EPI_RESID, p, gws, s));
         }
         {
             Timed t(m, PB_K_LN);
@@ -645,7 +648,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             p.X = u; p.ldx = d; p.W = m->ltensor(l, PB_T_W1); p.ldw = d; p.M = N; p.N = F; p.K1 = d;
             p.bias = m->ltensor(l, PB_T_B1);
             p.C = hbuf; p.ldc = F;
-            HIP_TRY(pb::launch_gemm(dt, 2, pb::EPI_RELU, p, s));
+            HIP_TRY(pb::launch_gemm(dt, 2, pb::EPI_RELU, p, gws, s));
         }
         {
             Timed t(m, PB_K_GEMM_FC2);
@@ -653,7 +656,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             p.X = hbuf; p.ldx = F; p.W = m->ltensor(l, PB_T_W2); p.ldw = F; p.M = N; p.N = d; p.K1 = F;
             p.bias = m->ltensor(l, PB_T_B2);
             p.R = x; p.ldr = d;
-            HIP_TRY(pb::launch_gemm(dt, 3, pb::EPI_RESID, p, s));
+            HIP_TRY(pb::launch_gemm(dt, 3, pb::EPI_RESID, p, gws, s));
         }
     }
     float* zf = (float*)m->at(a.zf);
