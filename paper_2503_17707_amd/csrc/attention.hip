@@ -29,7 +29,7 @@ constexpr float LOG2E = 1.4426950408889634f;
 template <int HD>
 __device__ __forceinline__ int kswz(int row, int ch) {
     // K tile rows are HD*2 bytes = HD/8 chunks of 16 bytes
-    if (HD == 64) return ch ^ ((row & 7) ^ ((row >> 3) & 1));
+    if (HD == 64) return ch ^ (row & 7);
     return ch ^ (row & 15);
 }
 

@@ -6,13 +6,15 @@
 // four consecutive output features of one token: the epilogue writes 8-byte
 // (dt) or 16-byte (fp32 residual) vectors.
 //
-// Block: 256 threads = 4 waves in a 2 x 2 grid; block tile BM x BN (128 x 128,
-// or 64 x 64 for the LoRA shrink and for N not a multiple of 128), K tile 64.
-// Tiles go global -> registers -> LDS; one or two register sets keep the
-// loads of tiles t+1 (and t+2) in flight while tile t is multiplied from LDS
-// (two LDS stages, one barrier per K tile).  LDS rows are 128 bytes (64 elements) with
-// the 16-byte chunks XOR-swizzled so that the MFMA operand reads of 16
-// consecutive rows hit distinct banks.
+// Block tile BM x BN, K tile 64: 256 x 256 with 8 waves (2 x 4, two waves per
+// SIMD) when such tiles alone fill the GPU, else 128 x 128 with 4 waves
+// (2 x 2), and 64 x 64 for the LoRA shrink and for N not a multiple of 128.  Tiles go straight from
+// global memory into an S-stage LDS ring (LDS-DMA, no staging registers), so
+// S-1 tiles are in flight while one is multiplied; one barrier per K tile.
+// LDS rows are 128 bytes (64 elements) with the 16-byte chunks XOR-swizzled by
+// the row index so that the MFMA operand reads of 16 consecutive rows are free
+// of bank conflicts (the DMA writes the swizzle by choosing which chunk each
+// lane fetches).
 //
 // Block order: the hardware deals consecutive blocks round-robin to the 8
 // XCDs; the block id is remapped so that each XCD gets a contiguous run of
@@ -36,8 +38,11 @@ namespace pb {
 
 namespace {
 
-#ifndef PB_GEMM_PF128
-#define PB_GEMM_PF128 1  // prefetch depth of the 128 x 128 tiles
+#ifndef PB_GEMM_STAGES
+#define PB_GEMM_STAGES 4  // LDS ring depth of the 128 x 128 tiles
+#endif
+#ifndef PB_GEMM_BIG
+#define PB_GEMM_BIG 1  // 256 x 256 tiles (8 waves) when they alone fill the GPU
 #endif
 #ifndef PB_GEMM_MIN_KT
 #define PB_GEMM_MIN_KT 8  // fewest K tiles a split-K block gets
@@ -47,9 +52,10 @@ constexpr int BK = 64;
 constexpr int ROW_BYTES = BK * 2;
 constexpr int GROUP_M = 8;
 
-__device__ __forceinline__ int swz(int row, int ch) {
-    return ch ^ ((row & 7) ^ ((row >> 3) & 1));
-}
+// Physical 16-byte chunk of logical chunk ch in LDS row `row`.  chunk ^ (row & 7)
+// measured conflict-free on gfx950 for the operand reads (16 rows, one chunk
+// per lane group) with the bank-conflict counter.
+__device__ __forceinline__ int swz(int row, int ch) { return ch ^ (row & 7); }
 
 // Epilogue of four consecutive output features n..n+3 of token m.
 template <typename T, int EPI>
@@ -93,18 +99,49 @@ struct SplitArgs {
     float* ws;      // [splits][M][N] fp32 partials when splits > 1
 };
 
-template <typename T, int EPI, int BM, int BN, int ROLE, int PF>
-__global__ __launch_bounds__(256) void gemm_kernel(GemmParams p, SplitArgs sa) {
+// One 16-byte global -> LDS copy per lane (LDS-DMA, global_load_lds_dwordx4):
+// lane i writes bytes [16 i, 16 i + 16) after the wave-uniform LDS address
+// lds_base.  Issued from inline assembly so that the compiler, which would
+// otherwise drain every outstanding load before the next LDS read, leaves the
+// waiting to the explicit s_waitcnt of the pipeline below; later
+// compiler-placed waits only ever wait for more, never less.
+// M0 is saved and restored around the copy, so the compiler's own use of M0
+// is never disturbed.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "global_load_lds_dwordx4 %2, off\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds_base), "v"(gptr)
+        : "memory");
+}
+
+// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <typename T, int EPI, int BM, int BN, int WGM, int WGN, int ROLE, int S>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmParams p, SplitArgs sa) {
     typedef typename Mfma<T>::vec8 vec8;
-    constexpr int WM = BM / 2, WN = BN / 2;     // wave tile
+    constexpr int NW = WGM * WGN;               // waves per block
+    constexpr int WM = BM / WGM, WN = BN / WGN;  // wave tile
     constexpr int MF = WM / 16, NF = WN / 16;   // 16x16 fragments per wave
-    constexpr int XL = BM * 8 / 256, WL = BN * 8 / 256;  // 16-byte loads per thread
+    constexpr int NL = (BM + BN) / (8 * NW);    // LDS-DMA instructions per wave per K tile
+    constexpr int NLX = BM / (8 * NW);          // ... of which carry X rows
     constexpr int STAGE = (BM + BN) * ROW_BYTES;
+    static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "DMA slots split into X and W");
+    static_assert(S >= 2 && (S - 2) * NL < 64, "pipeline depth");
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave & 1, wn = wave >> 1;
+    const int wm = wave % WGM, wn = wave / WGM;
     const int tiles_m = (p.M + BM - 1) / BM;
     const int tiles_n = (p.N + BN - 1) / BN;
     const int tiles = tiles_m * tiles_n;
@@ -122,72 +159,58 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p, SplitArgs sa) {
     const int tn = (tile % per_group) / gsize;
     const int m0 = tm * BM, n0 = tn * BN;
 
-    const T* X = (const T*)p.X;
-    const T* W = (const T*)p.W;
     const int nk1 = p.K1 / BK;
     int nk2 = 0;
-    const T* X2 = nullptr;
+    const T* X2 = (const T*)p.X2;
     if (p.K2 > 0) {
         const int g = n0 / p.group;
         if ((p.k2_mask >> g) & 1u) {
             nk2 = p.K2 / BK;
-            X2 = (const T*)p.X2 + (int64_t)g * p.x2_group_stride;
+            X2 += (int64_t)g * p.x2_group_stride;
         }
     }
-    const T* W2 = (const T*)p.W2;
     // K-tile range of this split
     const int t_begin = split * sa.kt_split;
     const int t_end = (split == sa.splits - 1) ? nk1 + nk2 : min(nk1, t_begin + sa.kt_split);
     const int nk = t_end - t_begin;
 
-    // per-thread load coordinates (row, 16-byte chunk) of the X and W tiles;
-    // element offsets fit in 31 bits (checked by the launcher)
-    int xoff[XL], woff[WL], xs[XL], ws[WL];
+    // DMA instruction j of this wave fills LDS rows 8g .. 8g+7, g = wave + NW j;
+    // rows < BM hold X (tokens), the rest W (output features): slots j < NLX.
+    // Lane i writes row 8g + i/8, physical chunk i%8, which holds logical K
+    // chunk (i%8) ^ (row & 7).  Element offsets fit in 31 bits (checked by the
+    // launcher); off1 addresses the base operands, off2 the LoRA ones.
+    const int lrow = lane >> 3;
+    int off1[NL], off2[NL];
 #pragma unroll
-    for (int i = 0; i < XL; ++i) {
-        const int c = tid + 256 * i, row = c >> 3, ch = c & 7;
-        const int m = min(m0 + row, p.M - 1);
-        xoff[i] = m * (int)p.ldx + ch * 8;
-        xs[i] = row * ROW_BYTES + (swz(row, ch) << 4);
-    }
-#pragma unroll
-    for (int i = 0; i < WL; ++i) {
-        const int c = tid + 256 * i, row = c >> 3, ch = c & 7;
-        const int n = min(n0 + row, p.N - 1);
-        woff[i] = n * (int)p.ldw + ch * 8;
-        ws[i] = BM * ROW_BYTES + row * ROW_BYTES + (swz(row, ch) << 4);
-    }
-
-    u32x4 rx0[XL], rw0[WL], rx1[XL], rw1[WL];
-    auto load = [&](int t, u32x4 (&rx)[XL], u32x4 (&rw)[WL]) {
-        if (t < nk1) {
-            const int k = t * BK;
-#pragma unroll
-            for (int i = 0; i < XL; ++i) rx[i] = *(const u32x4*)(X + xoff[i] + k);
-#pragma unroll
-            for (int i = 0; i < WL; ++i) rw[i] = *(const u32x4*)(W + woff[i] + k);
-        } else {  // LoRA expand tiles
-            const int k = (t - nk1) * BK;
-#pragma unroll
-            for (int i = 0; i < XL; ++i) {
-                const int c = tid + 256 * i;
-                const int m = min(m0 + (c >> 3), p.M - 1);
-                rx[i] = *(const u32x4*)(X2 + m * (int)p.ldx2 + (c & 7) * 8 + k);
-            }
-#pragma unroll
-            for (int i = 0; i < WL; ++i) {
-                const int c = tid + 256 * i;
-                const int n = min(n0 + (c >> 3), p.N - 1);
-                rw[i] = *(const u32x4*)(W2 + n * (int)p.ldw2 + (c & 7) * 8 + k);
-            }
+    for (int j = 0; j < NL; ++j) {
+        const int row = 8 * (wave + NW * j) + lrow;
+        const int ch = swz(row, lane & 7);
+        if (j < NLX) {
+            const int m = min(m0 + row, p.M - 1);
+            off1[j] = m * (int)p.ldx + ch * 8;
+            off2[j] = m * (int)p.ldx2 + ch * 8;
+        } else {
+            const int n = min(n0 + row - BM, p.N - 1);
+            off1[j] = n * (int)p.ldw + ch * 8;
+            off2[j] = n * (int)p.ldw2 + ch * 8;
         }
-    };
-    auto store = [&](int buf, const u32x4 (&rx)[XL], const u32x4 (&rw)[WL]) {
-        uint8_t* s = smem + buf * STAGE;
+    }
+    const T* Xb = (const T*)p.X;
+    const T* Wb = (const T*)p.W;
+    const T* W2 = (const T*)p.W2;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
+    auto issue = [&](int t, int stage) {
+        const uint32_t sbase = lds0 + stage * STAGE;
+        const bool base = t < nk1;
+        const T* xp = base ? Xb : X2;
+        const T* wp = base ? Wb : W2;
+        const int k = (base ? t : t - nk1) * BK;
 #pragma unroll
-        for (int i = 0; i < XL; ++i) *(u32x4*)(s + xs[i]) = rx[i];
-#pragma unroll
-        for (int i = 0; i < WL; ++i) *(u32x4*)(s + ws[i]) = rw[i];
+        for (int j = 0; j < NL; ++j) {
+            const int off = (base ? off1[j] : off2[j]) + k;
+            dma16((j < NLX ? xp : wp) + off,
+                  sbase + (uint32_t)__builtin_amdgcn_readfirstlane((wave + NW * j) * 1024));
+        }
     };
 
     f32x4 acc[NF][MF];
@@ -197,66 +220,43 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmParams p, SplitArgs sa) {
         for (int j = 0; j < MF; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     const int lr = lane & 15, lg = lane >> 4;
-    // operand read offsets inside a stage, for k step kk (0/1) of the 64-wide tile
-    auto aoff = [&](int kk, int i) {
-        const int row = wn * WN + i * 16 + lr, ch = kk * 4 + lg;
-        return BM * ROW_BYTES + row * ROW_BYTES + (swz(row, ch) << 4);
-    };
-    auto boff = [&](int kk, int j) {
-        const int row = wm * WM + j * 16 + lr, ch = kk * 4 + lg;
-        return row * ROW_BYTES + (swz(row, ch) << 4);
-    };
-    auto compute = [&](int buf) {
-        const uint8_t* s = smem + buf * STAGE;
+    auto compute = [&](int stage) {
+        const uint8_t* s = smem + stage * STAGE;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
+            const int ch = kk * 4 + lg;
             vec8 b[MF];
 #pragma unroll
-            for (int j = 0; j < MF; ++j) b[j] = as_vec8<T>(*(const u32x4*)(s + boff(kk, j)));
+            for (int j = 0; j < MF; ++j) {
+                const int row = wm * WM + j * 16 + lr;
+                b[j] = as_vec8<T>(*(const u32x4*)(s + row * ROW_BYTES + (swz(row, ch) << 4)));
+            }
 #pragma unroll
             for (int i = 0; i < NF; ++i) {
-                const vec8 a = as_vec8<T>(*(const u32x4*)(s + aoff(kk, i)));
+                const int row = BM + wn * WN + i * 16 + lr;
+                const vec8 a = as_vec8<T>(*(const u32x4*)(s + row * ROW_BYTES + (swz(row, ch) << 4)));
 #pragma unroll
                 for (int j = 0; j < MF; ++j) acc[i][j] = Mfma<T>::mma(a, b[j], acc[i][j]);
             }
         }
     };
 
-    if constexpr (PF == 1) {
-        // tile t+1 in registers while tile t is multiplied
-        if (nk > 0) {
-            load(t_begin, rx0, rw0);
-            store(0, rx0, rw0);
-        }
+    // S-stage ring: tiles t+1 .. t+S-1 are in flight while tile t is multiplied.
+    // Steady state first (branch-free), then the tail that drains the ring.
+#pragma unroll
+    for (int q = 0; q < S - 1; ++q)
+        if (q < nk) issue(t_begin + q, q);
+    int t = 0;
+    for (; t + S - 1 < nk; ++t) {
+        wait_vmcnt<(S - 2) * NL>();  // tiles t+1 .. t+S-2 may still fly
+        __syncthreads();             // tile t visible to all waves; stage of tile t-1 free
+        issue(t_begin + t + S - 1, (t + S - 1) % S);
+        compute(t % S);
+    }
+    for (; t < nk; ++t) {
+        wait_vmcnt<0>();
         __syncthreads();
-        for (int t = 0; t < nk; ++t) {
-            if (t + 1 < nk) load(t_begin + t + 1, rx0, rw0);
-            compute(t & 1);
-            if (t + 1 < nk) store((t + 1) & 1, rx0, rw0);
-            __syncthreads();
-        }
-    } else {
-        // tiles t+1 and t+2 in registers while tile t is multiplied
-        if (nk > 0) {
-            load(t_begin, rx0, rw0);
-            if (nk > 1) load(t_begin + 1, rx1, rw1);
-            store(0, rx0, rw0);
-            if (nk > 2) load(t_begin + 2, rx0, rw0);
-        }
-        __syncthreads();
-        for (int t = 0; t < nk; t += 2) {
-            // even step: compute stage 0; set 1 holds tile t+1, set 0 tile t+2
-            compute(0);
-            if (t + 1 < nk) store(1, rx1, rw1);
-            if (t + 3 < nk) load(t_begin + t + 3, rx1, rw1);
-            __syncthreads();
-            if (t + 1 >= nk) break;
-            // odd step: compute stage 1; set 0 holds tile t+2, set 1 tile t+3
-            compute(1);
-            if (t + 2 < nk) store(0, rx0, rw0);
-            if (t + 4 < nk) load(t_begin + t + 4, rx0, rw0);
-            __syncthreads();
-        }
+        compute(t % S);
     }
 
     // epilogue: lane holds n = nb + 4*lg + r (r = 0..3) of token m
@@ -296,12 +296,12 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p, SplitA
     epilogue4<T, EPI>(p, m, n, v);
 }
 
-template <typename T, int EPI, int BM, int BN, int ROLE, int PF>
+template <typename T, int EPI, int BM, int BN, int WGM, int WGN, int ROLE, int S>
 hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t s) {
-    constexpr int LDS = 2 * (BM + BN) * ROW_BYTES;
+    constexpr int LDS = S * (BM + BN) * ROW_BYTES;
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<T, EPI, BM, BN, ROLE, PF>,
+        hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<T, EPI, BM, BN, WGM, WGN, ROLE, S>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
         if (e != hipSuccess) return e;
         attr_set = true;
@@ -323,7 +323,8 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t
     // the LoRA tiles); S = ceil(nk1 / kt_split) leaves no split empty
     sa.splits = (nk1 + sa.kt_split - 1) / sa.kt_split;
     sa.ws = (float*)wsp.ws;
-    hipLaunchKernelGGL((gemm_kernel<T, EPI, BM, BN, ROLE, PF>), dim3(tiles * sa.splits), dim3(256), LDS, s,
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, BM, BN, WGM, WGN, ROLE, S>), dim3(tiles * sa.splits),
+                       dim3(64 * WGM * WGN), LDS, s,
                        p, sa);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || sa.splits == 1) return e;
@@ -335,8 +336,11 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t
 
 template <typename T, int EPI, int ROLE>
 hipError_t launch_tiles(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t s) {
-    if (p.N % 128 == 0) return launch_cfg<T, EPI, 128, 128, ROLE, PB_GEMM_PF128>(p, wsp, s);
-    return launch_cfg<T, EPI, 64, 64, ROLE, 2>(p, wsp, s);
+    const long t256 = (long)((p.M + 255) / 256) * ((p.N + 255) / 256);
+    if (PB_GEMM_BIG && p.N % 256 == 0 && t256 >= 256)
+        return launch_cfg<T, EPI, 256, 256, 2, 4, ROLE, 2>(p, wsp, s);
+    if (p.N % 128 == 0) return launch_cfg<T, EPI, 128, 128, 2, 2, ROLE, PB_GEMM_STAGES>(p, wsp, s);
+    return launch_cfg<T, EPI, 64, 64, 2, 2, ROLE, 4>(p, wsp, s);
 }
 
 template <typename T>
@@ -346,7 +350,7 @@ hipError_t launch_typed(int role, const GemmParams& p, const GemmWorkspace& wsp,
         case 1: return launch_tiles<T, EPI_RESID, 1>(p, wsp, s);
         case 2: return launch_tiles<T, EPI_RELU, 2>(p, wsp, s);
         case 3: return launch_tiles<T, EPI_RESID, 3>(p, wsp, s);
-        case 4: return launch_cfg<T, EPI_SHRINK, 64, 64, 4, 2>(p, wsp, s);
+        case 4: return launch_cfg<T, EPI_SHRINK, 64, 64, 2, 2, 4, 4>(p, wsp, s);
         default: break;
     }
     return hipErrorInvalidValue;
