@@ -173,7 +173,7 @@ const char* pb_last_error(void);
 
 /* ---- loader and measurement controls ------------------------------------- */
 
-/* Largest single hipMemcpyAsync the loader issues (default 64 MiB, min 1 MiB). */
+/* Largest single hipMemcpyAsync the loader issues (default 256 MiB, min 1 MiB). */
 int pb_set_chunk_bytes(pb_model* m, size_t bytes);
 
 /* Bytes and elapsed milliseconds (copy-stream events, first copy start to last

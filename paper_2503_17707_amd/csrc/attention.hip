@@ -2,9 +2,10 @@
 // prompt tokens through self-attention; a prefill is causal, token j sees
 // tokens 0..j), flash-style: the T x T score matrix is never stored.
 //
-// Block = 4 waves = 64 queries of one (sequence, head); each wave owns 16
-// queries.  Key/value blocks of 64 rows are staged in LDS (K row-major, V
-// transposed) and consumed with v_mfma_f32_16x16x32_{f16,bf16}:
+// Block = 4 waves of one (sequence, head); each wave owns 16 or 32 queries.
+// Key/value tiles of 64 rows arrive row-major in a two-stage LDS ring by
+// LDS-DMA (the next tile loads while this one is used) and are consumed with
+// v_mfma_f32_16x16x32_{f16,bf16}:
 //
 //   S^T[key, query] = K Q^T      A operand = K rows, B operand = the wave's Q
 //                                 (held in registers for the whole kernel)
@@ -14,7 +15,8 @@
 // query (lane % 16), so the online softmax (running max m, running sum l, in
 // fp32) needs only cross-lane reductions over the 4 lane groups and no
 // transposition of P: the 8 keys a lane contributes to one P^T operand are the
-// 8 scores it already holds, and V^T is read in the same key order.
+// 8 scores it already holds.  The V^T operand is read from the row-major V
+// tile with transposing LDS reads (ds_read_b64_tr_b16) in the same key order.
 //
 // Blocks run heaviest-first (the last query block sees the most keys).
 #include "common.h"
@@ -24,166 +26,268 @@ namespace pb {
 
 namespace {
 
-constexpr float LOG2E = 1.4426950408889634f;
+#ifndef PB_ATTN_QW32
+#define PB_ATTN_QW32 1  // allow 32 queries per wave
+#endif
 
-template <int HD>
-__device__ __forceinline__ int kswz(int row, int ch) {
-    // K tile rows are HD*2 bytes = HD/8 chunks of 16 bytes
-    if (HD == 64) return ch ^ (row & 7);
-    return ch ^ (row & 15);
+constexpr float LOG2E = 1.4426950408889634f;
+constexpr int BKV = 64;  // keys per tile
+
+// One 16-byte global -> LDS copy per lane (LDS-DMA): lane i writes bytes
+// [16 i, 16 i + 16) after the wave-uniform LDS address lds_base.  M0 is saved
+// and restored; waiting is left to the explicit s_waitcnt below.
+__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "global_load_lds_dwordx4 %2, off\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds_base), "v"(gptr)
+        : "memory");
 }
 
-template <typename T, int HD>
-__global__ __launch_bounds__(256) void attention_kernel(const T* __restrict__ qkv,
+__device__ __forceinline__ void wait_vmcnt0() {
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
+}
+
+// 16-byte chunk permutations of a K or V tile row (key = row): K is read as
+// 16 consecutive rows at one chunk, V by transposing 8-byte reads of four
+// consecutive rows at two neighbouring chunks.
+__device__ __forceinline__ int kswz(int row, int ch) { return ch ^ (row & 7); }
+__device__ __forceinline__ int vswz(int row, int ch) { return ch ^ ((row & 3) << 1); }
+
+// Transposing LDS read (ds_read_b64_tr_b16): within each group of 16 lanes,
+// lane i receives element i % 4 of the 8-byte segments addressed by lanes
+// 4 j + i / 4, j = 0..3 (layout checked on gfx950 with an in-bounds probe).
+template <typename T>
+__device__ __forceinline__ u32x2 read_tr16(const uint8_t* p) {
+    typedef short s16x4 __attribute__((ext_vector_type(4)));
+    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4*)(p));
+    return __builtin_bit_cast(u32x2, v);
+}
+
+template <typename T, int HD, int QW>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(QW == 32 ? 2 : 1)))
+void attention_kernel(const T* __restrict__ qkv,
                                                        T* __restrict__ out, int T_len, int H) {
     typedef typename Mfma<T>::vec8 vec8;
-    constexpr int BQ = 64, BKV = 64;
-    constexpr int CS = HD / 32;   // 32-wide k steps over head_dim
-    constexpr int CT = HD / 16;   // 16-row tiles of O^T
-    constexpr int KCH = HD / 8;   // 16-byte chunks per K row
-    __shared__ __attribute__((aligned(16))) uint8_t sK[BKV * HD * 2];
-    __shared__ __attribute__((aligned(16))) uint8_t sV[HD * BKV * 2];  // V^T: [HD][64 keys]
+    constexpr int BQ = 4 * QW;         // queries per block (4 waves)
+    constexpr int NQG = QW / 16;       // 16-query groups per wave
+    constexpr int CS = HD / 32;        // 32-wide k steps over head_dim
+    constexpr int CT = HD / 16;        // 16-row tiles of O^T
+    constexpr int RB = HD * 2;         // bytes per K/V row
+    constexpr int CPR = RB / 16;       // 16-byte chunks per row
+    constexpr int TILE = BKV * RB;     // bytes per K or V tile
+    constexpr int STAGE = 2 * TILE;    // K then V
+    constexpr int NI = STAGE / 1024;   // 1 KB DMA instructions per stage
+    constexpr int NL = NI / 4;         // ... per wave
+    constexpr int RPI = 1024 / RB;     // rows per DMA instruction
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
     const int d = H * HD;
     const int64_t ld = 3 * (int64_t)d;
     const int nqb = (T_len + BQ - 1) / BQ;
-    const int qb = nqb - 1 - (int)blockIdx.x;
+    const int qb = nqb - 1 - (int)blockIdx.x;  // heaviest blocks first
     const int h = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int lr = lane & 15, lg = lane >> 4;
     const int64_t row0 = (int64_t)b * T_len;
     const T* Qb = qkv + h * HD;
-    const T* Kb = qkv + d + h * HD;
-    const T* Vb = qkv + 2 * d + h * HD;
 
-    const int q_idx = qb * BQ + wave * 16 + lr;
-    const int q_row = min(q_idx, T_len - 1);
-    vec8 qf[CS];
+    // Q^T operands stay in registers: query = q0 + 16 qg + lr
+    const int q0 = qb * BQ + wave * QW;
+    vec8 qf[NQG][CS];
 #pragma unroll
-    for (int cs = 0; cs < CS; ++cs)
-        qf[cs] = as_vec8<T>(*(const u32x4*)(Qb + (row0 + q_row) * ld + cs * 32 + 8 * lg));
+    for (int qg = 0; qg < NQG; ++qg) {
+        const int qr = min(q0 + 16 * qg + lr, T_len - 1);
+#pragma unroll
+        for (int cs = 0; cs < CS; ++cs)
+            qf[qg][cs] = as_vec8<T>(*(const u32x4*)(Qb + (row0 + qr) * ld + cs * 32 + 8 * lg));
+    }
 
-    f32x4 o[CT];
+    // DMA slot j of this wave: instruction I = wave + 4 j of the stage (K tile
+    // first, then V); lane i fills row RPI * (I % (NI / 2)) + i / CPR, physical
+    // chunk i % CPR, i.e. logical chunk (i % CPR) ^ permutation of that row.
+    const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
+    auto issue = [&](int kb, int stage) {
+        const uint32_t sbase = lds0 + stage * STAGE;
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct) o[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float m_run = -INFINITY, l_run = 0.f;
-
-    const int nkb = qb + 1;
-    for (int kb = 0; kb < nkb; ++kb) {
-        __syncthreads();
-        // stage K (row-major, swizzled) and V^T (swizzled 8-byte units)
-#pragma unroll
-        for (int i = 0; i < BKV * KCH / 256; ++i) {
-            const int c = tid + 256 * i, row = c / KCH, ch = c % KCH;
+        for (int j = 0; j < NL; ++j) {
+            const int I = wave + 4 * j;
+            const bool isv = I >= NI / 2;
+            const int row = RPI * (I % (NI / 2)) + lane / CPR;
+            const int pch = lane % CPR;
+            const int ch = isv ? vswz(row, pch) : kswz(row, pch);
             const int key = min(kb * BKV + row, T_len - 1);
-            const u32x4 kv = *(const u32x4*)(Kb + (row0 + key) * ld + ch * 8);
-            *(u32x4*)(sK + row * HD * 2 + (kswz<HD>(row, ch) << 4)) = kv;
-            const u32x4 vv = *(const u32x4*)(Vb + (row0 + key) * ld + ch * 8);
-            T ve[8];
-            __builtin_memcpy(ve, &vv, 16);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int cc = ch * 8 + e;  // column of V = row of V^T
-                const int unit = (row >> 2) ^ (cc & 15);
-                *(T*)(sV + cc * (BKV * 2) + unit * 8 + (row & 3) * 2) = ve[e];
-            }
+            const T* src = qkv + (row0 + key) * ld + (isv ? 2 * d : d) + h * HD + ch * 8;
+            dma16(src, sbase + (uint32_t)__builtin_amdgcn_readfirstlane(I * 1024));
         }
-        __syncthreads();
+    };
 
-        // S^T tiles: key = kb*64 + 16*jt + 4*lg + r, query = q_idx
-        f32x4 s[4];
+    f32x4 o[NQG][CT];
+    float m_run[NQG], l_run[NQG];
+#pragma unroll
+    for (int qg = 0; qg < NQG; ++qg) {
+        m_run[qg] = -INFINITY;
+        l_run[qg] = 0.f;
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) o[qg][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+    // keys needed by this block: those <= its last query (and < T)
+    const int nkb = min((T_len + BKV - 1) / BKV, ((qb + 1) * BQ + BKV - 1) / BKV);
+    issue(0, 0);
+    for (int kb = 0; kb < nkb; ++kb) {
+        wait_vmcnt0();
+        __syncthreads();  // tile kb visible; stage of tile kb-1 free
+        if (kb + 1 < nkb) issue(kb + 1, (kb + 1) & 1);
+        const uint8_t* sK = smem + (kb & 1) * STAGE;
+        const uint8_t* sV = sK + TILE;
+
+        // S^T tiles: key = kb*64 + 16 jt + 4 lg + r, query = q0 + 16 qg + lr
+        f32x4 sc[NQG][4];
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) {
-            s[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
             const int row = jt * 16 + lr;
+            vec8 kf[CS];
 #pragma unroll
-            for (int cs = 0; cs < CS; ++cs) {
-                const int ch = cs * 4 + lg;
-                const vec8 kf = as_vec8<T>(*(const u32x4*)(sK + row * HD * 2 + (kswz<HD>(row, ch) << 4)));
-                s[jt] = Mfma<T>::mma(kf, qf[cs], s[jt]);
+            for (int cs = 0; cs < CS; ++cs)
+                kf[cs] = as_vec8<T>(*(const u32x4*)(sK + row * RB + (kswz(row, cs * 4 + lg) << 4)));
+#pragma unroll
+            for (int qg = 0; qg < NQG; ++qg) {
+                sc[qg][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int cs = 0; cs < CS; ++cs) sc[qg][jt] = Mfma<T>::mma(kf[cs], qf[qg][cs], sc[qg][jt]);
             }
         }
-        // mask (causal and ragged tail) and block maximum
-        float mx = -INFINITY;
-        const bool diag = (kb == qb) || ((kb + 1) * BKV > T_len);
+        // online softmax per query (fp32); P rounded to dt as it enters the MFMA,
+        // and the running sum adds the rounded values
+        const bool edge = ((kb + 1) * BKV > q0) || ((kb + 1) * BKV > T_len);
+        vec8 pf[NQG][2];
 #pragma unroll
-        for (int jt = 0; jt < 4; ++jt)
+        for (int qg = 0; qg < NQG; ++qg) {
+            const int q_idx = q0 + 16 * qg + lr;
+            if (edge) {  // wave-uniform: only tiles that reach past a query or past T
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int key = kb * BKV + jt * 16 + 4 * lg + r;
-                if (diag && (key > q_idx || key >= T_len)) s[jt][r] = -INFINITY;
-                mx = fmaxf(mx, s[jt][r]);
+                for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int key = kb * BKV + jt * 16 + 4 * lg + r;
+                        const bool masked = (key > q_idx) | (key >= T_len);
+                        sc[qg][jt][r] = masked ? -INFINITY : sc[qg][jt][r];
+                    }
             }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = fmaxf(m_run, mx);  // finite: key kb*64 <= q_idx is always allowed
-        const float alpha = exp2f((m_run - m_new) * LOG2E);
-        const float mb = m_new * LOG2E;
-        // probabilities, rounded to dt as they enter the MFMA; the sum uses the rounded values
-        T pt[4][4];
-        float psum = 0.f;
+            float mx = -INFINITY;
 #pragma unroll
-        for (int jt = 0; jt < 4; ++jt)
+            for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const T pv = (T)exp2f(s[jt][r] * LOG2E - mb);
-                pt[jt][r] = pv;
-                psum += (float)pv;
-            }
-        psum += __shfl_xor(psum, 16, 64);
-        psum += __shfl_xor(psum, 32, 64);
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
+                for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[qg][jt][r]);
+            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            // key kb*64 <= q_idx always holds for a computed tile, so m_new is finite
+            const float m_new = fmaxf(m_run[qg], mx);
+            // arguments are <= 0: the hardware exp2 (v_exp_f32) is exact enough and
+            // maps -inf to 0
+            const float alpha = __builtin_amdgcn_exp2f((m_run[qg] - m_new) * LOG2E);
+            const float mb = m_new * LOG2E;
+            T pt[4][4];
+            float psum = 0.f;
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-            o[ct][0] *= alpha;
-            o[ct][1] *= alpha;
-            o[ct][2] *= alpha;
-            o[ct][3] *= alpha;
-        }
-        // O^T += V^T P^T over two 32-key steps; k index 8*lg + 4*hh + r <-> key 32*ks + 16*hh + 4*lg + r
+            for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            T pk[8];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                pk[r] = pt[2 * ks][r];
-                pk[4 + r] = pt[2 * ks + 1][r];
-            }
-            u32x4 praw;
-            __builtin_memcpy(&praw, pk, 16);
-            const vec8 pf = as_vec8<T>(praw);
+                for (int r = 0; r < 4; ++r) {
+                    const T pv = (T)__builtin_amdgcn_exp2f(sc[qg][jt][r] * LOG2E - mb);
+                    pt[jt][r] = pv;
+                    psum += (float)pv;
+                }
+            psum += __shfl_xor(psum, 16, 64);
+            psum += __shfl_xor(psum, 32, 64);
+            l_run[qg] = l_run[qg] * alpha + psum;
+            m_run[qg] = m_new;
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct) {
-                const int cc = ct * 16 + lr;
-                const int u0 = ((32 * ks + 4 * lg) >> 2) ^ (cc & 15);
-                const int u1 = ((32 * ks + 16 + 4 * lg) >> 2) ^ (cc & 15);
-                const u32x2 v0 = *(const u32x2*)(sV + cc * (BKV * 2) + u0 * 8);
-                const u32x2 v1 = *(const u32x2*)(sV + cc * (BKV * 2) + u1 * 8);
-                const u32x4 vraw = u32x4{v0[0], v0[1], v1[0], v1[1]};
-                o[ct] = Mfma<T>::mma(as_vec8<T>(vraw), pf, o[ct]);
+                o[qg][ct][0] *= alpha;
+                o[qg][ct][1] *= alpha;
+                o[qg][ct][2] *= alpha;
+                o[qg][ct][3] *= alpha;
+            }
+            // P^T operand of key step ks: k index 8 lg + 4 hh + r <-> key 32 ks + 16 hh + 4 lg + r
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                T pk[8];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    pk[r] = pt[2 * ks][r];
+                    pk[4 + r] = pt[2 * ks + 1][r];
+                }
+                u32x4 praw;
+                __builtin_memcpy(&praw, pk, 16);
+                pf[qg][ks] = as_vec8<T>(praw);
+            }
+        }
+        // O^T += V^T P^T: the V^T operand (row c, k index 8 lg + 4 hh + j) comes from two
+        // transposing reads; lane 4 j + q of a 16-lane group addresses row
+        // 32 ks + 16 hh + 4 lg + j, columns 16 ct + 4 q .. + 3
+        const int tj = lr >> 2, tq = lr & 3;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                u32x2 v[2];
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh) {
+                    const int row = 32 * ks + 16 * hh + 4 * lg + tj;
+                    const int col = 16 * ct + 4 * tq;  // element column
+                    const int ch = col >> 3;
+                    v[hh] = read_tr16<T>(sV + row * RB + (vswz(row, ch) << 4) + (col & 7) * 2);
+                }
+                const vec8 vf = as_vec8<T>(u32x4{v[0][0], v[0][1], v[1][0], v[1][1]});
+#pragma unroll
+                for (int qg = 0; qg < NQG; ++qg) o[qg][ct] = Mfma<T>::mma(vf, pf[qg][ks], o[qg][ct]);
             }
         }
     }
 
-    if (q_idx < T_len) {
-        const float inv = 1.f / l_run;
+#pragma unroll
+    for (int qg = 0; qg < NQG; ++qg) {
+        const int q_idx = q0 + 16 * qg + lr;
+        if (q_idx >= T_len) continue;
+        const float inv = 1.f / l_run[qg];
         T* orow = out + (row0 + q_idx) * (int64_t)d + h * HD;
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) {
             const int c = ct * 16 + 4 * lg;
-            *(u32x2*)(orow + c) = pack4<T>(o[ct][0] * inv, o[ct][1] * inv, o[ct][2] * inv,
-                                           o[ct][3] * inv);
+            *(u32x2*)(orow + c) = pack4<T>(o[qg][ct][0] * inv, o[qg][ct][1] * inv,
+                                           o[qg][ct][2] * inv, o[qg][ct][3] * inv);
         }
     }
 }
 
-template <typename T, int HD>
+template <typename T, int HD, int QW>
 hipError_t launch_hd(const void* qkv, void* out, int B, int T_len, int H, hipStream_t s) {
-    dim3 grid((T_len + 63) / 64, H, B);
-    hipLaunchKernelGGL((attention_kernel<T, HD>), grid, dim3(256), 0, s, (const T*)qkv, (T*)out,
-                       T_len, H);
+    constexpr int LDS = 2 * 2 * BKV * HD * 2;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute((const void*)attention_kernel<T, HD, QW>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    dim3 grid((T_len + 4 * QW - 1) / (4 * QW), H, B);
+    hipLaunchKernelGGL((attention_kernel<T, HD, QW>), grid, dim3(256), LDS, s, (const T*)qkv,
+                       (T*)out, T_len, H);
     return hipGetLastError();
+}
+
+template <typename T, int HD>
+hipError_t launch_qw(const void* qkv, void* out, int B, int T_len, int H, hipStream_t s) {
+    // 32 queries per wave when 128-query blocks still give every CU work
+    const long blocks128 = (long)((T_len + 127) / 128) * H * B;
+    if (PB_ATTN_QW32 && blocks128 >= 512) return launch_hd<T, HD, 32>(qkv, out, B, T_len, H, s);
+    return launch_hd<T, HD, 16>(qkv, out, B, T_len, H, s);
 }
 
 }  // namespace
@@ -191,12 +295,13 @@ hipError_t launch_hd(const void* qkv, void* out, int B, int T_len, int H, hipStr
 hipError_t launch_attention(int dtype, const void* qkv, void* out, int B, int T_len, int H,
                             int hd, hipStream_t s) {
     if (B <= 0 || T_len <= 0) return hipSuccess;
+    if ((int64_t)B * T_len * 3 * H * hd >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
     if (dtype == 1) {
-        if (hd == 64) return launch_hd<_Float16, 64>(qkv, out, B, T_len, H, s);
-        if (hd == 128) return launch_hd<_Float16, 128>(qkv, out, B, T_len, H, s);
+        if (hd == 64) return launch_qw<_Float16, 64>(qkv, out, B, T_len, H, s);
+        if (hd == 128) return launch_qw<_Float16, 128>(qkv, out, B, T_len, H, s);
     } else {
-        if (hd == 64) return launch_hd<__bf16, 64>(qkv, out, B, T_len, H, s);
-        if (hd == 128) return launch_hd<__bf16, 128>(qkv, out, B, T_len, H, s);
+        if (hd == 64) return launch_qw<__bf16, 64>(qkv, out, B, T_len, H, s);
+        if (hd == 128) return launch_qw<__bf16, 128>(qkv, out, B, T_len, H, s);
     }
     return hipErrorInvalidValue;
 }

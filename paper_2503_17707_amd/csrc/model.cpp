@@ -222,7 +222,7 @@ struct pb_model {
     hipEvent_t ev_globals = nullptr, ev_lora = nullptr, ev_load0 = nullptr, ev_load1 = nullptr;
     bool streamed = false, lora_recorded = false;
     double last_load_bytes = 0;
-    size_t chunk_bytes = 64u << 20;
+    size_t chunk_bytes = 256u << 20;
     int delay_us = 0;
     // adapter slots
     bool slot_valid[MAX_SLOTS] = {};
