@@ -1,0 +1,52 @@
+/*
+ * pipeboost_ops.h -- kernel-level entry points of libpipeboost.so.
+ *
+ * Each call runs one kernel of the prefill (plus its split-K reduce where the
+ * launcher splits) on caller-provided device buffers, on the given stream,
+ * asynchronously.  They exist to test every kernel against the CPU oracle's
+ * component functions and to time kernels in isolation; the model API in
+ * pipeboost.h is the product path.  All pointers are device pointers, all
+ * matrices row-major with the reduction dimension contiguous; "dt" is
+ * bfloat16 (dtype 0) or IEEE binary16 (dtype 1).  Every call returns a
+ * pb_status (PB_EINVAL for unsupported shapes, PB_EHIP for launch failures,
+ * message in pb_last_error()).
+ */
+#ifndef PIPEBOOST_OPS_H
+#define PIPEBOOST_OPS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Projection GEMM Y = X W^T (fp32 accumulate) with an epilogue
+ * (Section 2.1: the decoder's linear layers; bias as in OPT):
+ *   epi 0: C = dt((Y + bias) * (n < qcols ? qscale : 1))   (q, k, v projection)
+ *   epi 1: C = dt(max(Y + bias, 0))                        (fc1 with ReLU)
+ *   epi 2: R += Y + bias, R fp32 [M, N] (ldr = N)           (o and fc2, residual)
+ * X [M, K] dt, W [N, K] dt, bias [N] dt, C [M, N] dt (ldc = N).  Requires
+ * N % 64 == 0 and K % 64 == 0.  workspace (fp32 scratch for split-K partials,
+ * may be NULL) of workspace_bytes. */
+int pb_op_gemm(int32_t dtype, int32_t epi, const void* X, const void* W, const void* bias,
+               void* C, float* R, int32_t M, int32_t N, int32_t K, float qscale, int32_t qcols,
+               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Causal multi-head self-attention over B sequences of T tokens (Section 2.1:
+ * prefill self-attention; token j attends to tokens 0..j).  qkv [B*T, 3*H*hd]
+ * dt with q already divided by sqrt(hd), out [B*T, H*hd] dt; hd in {64, 128}. */
+int pb_op_attention(int32_t dtype, const void* qkv, void* out, int32_t B, int32_t T,
+                    int32_t H, int32_t hd, void* stream);
+
+/* LayerNorm of rows of an fp32 matrix x [rows, d]: out = LN(x) * g + b with
+ * fp32 statistics (biased variance); g, b [d] dt; out [rows, d] dt, or fp32
+ * when out_f32 != 0.  d % 4 == 0, d <= 16384. */
+int pb_op_layernorm(int32_t dtype, const float* x, const void* g, const void* b, void* out,
+                    int32_t out_f32, int32_t rows, int32_t d, float eps, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PIPEBOOST_OPS_H */

@@ -87,6 +87,17 @@ _SIGS = {
     "pb_reset_kernel_timing": (ctypes.c_int, [ctypes.c_void_p]),
     "pb_poison_weights": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
     "pb_set_stream_delay_us": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
+    "pb_op_gemm": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                  ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_int32,
+                                  ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "pb_op_attention": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                       ctypes.c_int32, ctypes.c_void_p]),
+    "pb_op_layernorm": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                       ctypes.c_int32, ctypes.c_int32, ctypes.c_float,
+                                       ctypes.c_void_p]),
 }
 
 _lib = None
@@ -351,3 +362,40 @@ def attach_all(m: Model, hw: HostWeights):
     for a in used:
         blobs = hw.loras.get(a) or hw.add_lora(a)
         m.attach_lora(a, blobs, w.lora_rank, w.lora_alpha, hw.lora_mask())
+
+
+# ---- kernel-level entry points (include/pipeboost_ops.h) --------------------
+# Arguments are torch tensors on the GPU; the call is enqueued on `stream`
+# (a torch.cuda.Stream, default: the current stream).
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+
+    return ctypes.c_void_p((stream or torch.cuda.current_stream()).cuda_stream)
+
+
+def op_gemm(dtype: int, epi: int, X, W, bias, C=None, R=None, qscale: float = 1.0,
+            qcols: int = 0, workspace=None, stream=None):
+    M, K = X.shape
+    N = W.shape[0]
+    check(lib().pb_op_gemm(dtype, epi, _ptr(X), _ptr(W), _ptr(bias), _ptr(C), _ptr(R), M, N, K,
+                           qscale, qcols, _ptr(workspace),
+                           0 if workspace is None else workspace.numel() * workspace.element_size(),
+                           _stream(stream)))
+
+
+def op_attention(dtype: int, qkv, out, B: int, T: int, H: int, hd: int, stream=None):
+    check(lib().pb_op_attention(dtype, _ptr(qkv), _ptr(out), B, T, H, hd, _stream(stream)))
+
+
+def op_layernorm(dtype: int, x, g, b, out, eps: float = 1e-5, stream=None):
+    rows, d = x.shape
+    import torch
+
+    check(lib().pb_op_layernorm(dtype, _ptr(x), _ptr(g), _ptr(b), _ptr(out),
+                                1 if out.dtype == torch.float32 else 0, rows, d, eps,
+                                _stream(stream)))

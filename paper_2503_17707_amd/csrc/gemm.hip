@@ -6,9 +6,9 @@
 // four consecutive output features of one token: the epilogue writes 8-byte
 // (dt) or 16-byte (fp32 residual) vectors.
 //
-// Block tile BM x BN, K tile 64: 256 x 256 with 8 waves (2 x 4, two waves per
-// SIMD) when such tiles alone fill the GPU, else 128 x 128 with 4 waves
-// (2 x 2), and 64 x 64 for the LoRA shrink and for N not a multiple of 128.  Tiles go straight from
+// Block tile BM x BN, K tile 64: 256 x 256 or 128 x 128 with 8 waves (2 x 4,
+// two waves per SIMD, chosen by how many tiles the shape gives), and 64 x 64
+// with 4 waves for the LoRA shrink and for N not a multiple of 128.  Tiles go straight from
 // global memory into an S-stage LDS ring (LDS-DMA, no staging registers), so
 // S-1 tiles are in flight while one is multiplied; one barrier per K tile.
 // LDS rows are 128 bytes (64 elements) with the 16-byte chunks XOR-swizzled by
@@ -38,12 +38,6 @@ namespace pb {
 
 namespace {
 
-#ifndef PB_GEMM_STAGES
-#define PB_GEMM_STAGES 4  // LDS ring depth of the 128 x 128 tiles
-#endif
-#ifndef PB_GEMM_BIG
-#define PB_GEMM_BIG 1  // 256 x 256 tiles (8 waves) when they alone fill the GPU
-#endif
 #ifndef PB_GEMM_MIN_KT
 #define PB_GEMM_MIN_KT 8  // fewest K tiles a split-K block gets
 #endif
@@ -77,8 +71,11 @@ __device__ __forceinline__ void epilogue4(const GemmParams& p, int m, int n, f32
 #pragma unroll
     for (int r = 0; r < 4; ++r) y[r] = v[r] + (float)bb[r];
     if (EPI == EPI_QKV) {
-        const float sc = n < p.qcols ? p.qscale : 1.f;
-        *(u32x2*)((T*)p.C + (int64_t)m * p.ldc + n) = pack4<T>(y[0] * sc, y[1] * sc, y[2] * sc, y[3] * sc);
+        float sc[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sc[r] = n + r < p.qcols ? p.qscale : 1.f;
+        *(u32x2*)((T*)p.C + (int64_t)m * p.ldc + n) =
+            pack4<T>(y[0] * sc[0], y[1] * sc[1], y[2] * sc[2], y[3] * sc[3]);
     } else if (EPI == EPI_RELU) {
         *(u32x2*)((T*)p.C + (int64_t)m * p.ldc + n) =
             pack4<T>(fmaxf(y[0], 0.f), fmaxf(y[1], 0.f), fmaxf(y[2], 0.f), fmaxf(y[3], 0.f));
@@ -296,6 +293,83 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p, SplitA
     epilogue4<T, EPI>(p, m, n, v);
 }
 
+// Row-wise split-K reduce of a residual projection fused with the LayerNorm
+// that follows it: R[m] += (sum of partials in split order) + bias, then
+// ln_out[m] = dt(LN(R[m]) * g + b) with fp32 statistics.  One block per row.
+constexpr int RLN_MAXC = 16;  // float4 chunks per thread: N <= 16384
+
+template <typename T>
+__global__ __launch_bounds__(256) void splitk_resid_ln_kernel(GemmParams p, SplitArgs sa) {
+    __shared__ float red[4];
+    const int m = blockIdx.x;
+    const int nc = p.N / 4;
+    const int64_t stride = (int64_t)p.M * p.N;
+    float* xr = p.R + (int64_t)m * p.ldr;
+    const float* wr = sa.ws + (int64_t)m * p.N;
+    f32x4 v[RLN_MAXC];
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < RLN_MAXC; ++i) {
+        const int c = threadIdx.x + 256 * i;
+        if (c < nc) {
+            f32x4 a = *(const f32x4*)(wr + 4 * c);
+            for (int s = 1; s < sa.splits; ++s) {
+                const f32x4 w = *(const f32x4*)(wr + s * stride + 4 * c);
+                a[0] += w[0];
+                a[1] += w[1];
+                a[2] += w[2];
+                a[3] += w[3];
+            }
+            const u32x2 braw = *(const u32x2*)((const T*)p.bias + 4 * c);
+            T bb[4];
+            __builtin_memcpy(bb, &braw, 8);
+            f32x4 x = *(const f32x4*)(xr + 4 * c);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) x[r] += a[r] + (float)bb[r];
+            *(f32x4*)(xr + 4 * c) = x;
+            v[i] = x;
+            sum += (x[0] + x[1]) + (x[2] + x[3]);
+        }
+    }
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    sum = wave_sum(sum);
+    if (lane == 0) red[wave] = sum;
+    __syncthreads();
+    const float mean = (red[0] + red[1] + red[2] + red[3]) / (float)p.N;
+    __syncthreads();
+    float q = 0.f;
+#pragma unroll
+    for (int i = 0; i < RLN_MAXC; ++i) {
+        const int c = threadIdx.x + 256 * i;
+        if (c < nc)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float t = v[i][r] - mean;
+                q += t * t;
+            }
+    }
+    q = wave_sum(q);
+    if (lane == 0) red[wave] = q;
+    __syncthreads();
+    const float var = (red[0] + red[1] + red[2] + red[3]) / (float)p.N;
+    const float rstd = 1.0f / sqrtf(var + p.ln_eps);
+#pragma unroll
+    for (int i = 0; i < RLN_MAXC; ++i) {
+        const int c = threadIdx.x + 256 * i;
+        if (c < nc) {
+            const u32x2 graw = *(const u32x2*)((const T*)p.ln_g + 4 * c);
+            const u32x2 braw = *(const u32x2*)((const T*)p.ln_b + 4 * c);
+            T ga[4], ba[4];
+            __builtin_memcpy(ga, &graw, 8);
+            __builtin_memcpy(ba, &braw, 8);
+            float y[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) y[r] = (v[i][r] - mean) * rstd * (float)ga[r] + (float)ba[r];
+            *(u32x2*)((T*)p.ln_out + (int64_t)m * p.N + 4 * c) = pack4<T>(y[0], y[1], y[2], y[3]);
+        }
+    }
+}
+
 template <typename T, int EPI, int BM, int BN, int WGM, int WGN, int ROLE, int S>
 hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t s) {
     constexpr int LDS = S * (BM + BN) * ROW_BYTES;
@@ -328,6 +402,12 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t
                        p, sa);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || sa.splits == 1) return e;
+    if (EPI == EPI_RESID && p.ln_out && p.N <= 256 * 4 * RLN_MAXC) {
+        hipLaunchKernelGGL((splitk_resid_ln_kernel<T>), dim3(p.M), dim3(256), 0, s, p, sa);
+        e = hipGetLastError();
+        if (e == hipSuccess && p.ln_done) *p.ln_done = true;
+        return e;
+    }
     const int64_t groups = (int64_t)p.M * (p.N / 4);
     hipLaunchKernelGGL((splitk_reduce_kernel<T, EPI>), dim3((unsigned)((groups + 255) / 256)), dim3(256), 0,
                        s, p, sa);
@@ -336,10 +416,12 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t
 
 template <typename T, int EPI, int ROLE>
 hipError_t launch_tiles(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t s) {
-    const long t256 = (long)((p.M + 255) / 256) * ((p.N + 255) / 256);
-    if (PB_GEMM_BIG && p.N % 256 == 0 && t256 >= 256)
+    auto tiles = [&](int bm, int bn) { return (long)((p.M + bm - 1) / bm) * ((p.N + bn - 1) / bn); };
+    // 256 x 256 when those tiles fill the GPU, or half fill it over a long K
+    // (then split along K); else 128 x 128 (split along K when too few)
+    if (p.N % 256 == 0 && (tiles(256, 256) >= 256 || (tiles(256, 256) >= 128 && p.K1 >= 8192)))
         return launch_cfg<T, EPI, 256, 256, 2, 4, ROLE, 2>(p, wsp, s);
-    if (p.N % 128 == 0) return launch_cfg<T, EPI, 128, 128, 2, 2, ROLE, PB_GEMM_STAGES>(p, wsp, s);
+    if (p.N % 128 == 0) return launch_cfg<T, EPI, 128, 128, 2, 4, ROLE, 2>(p, wsp, s);
     return launch_cfg<T, EPI, 64, 64, 2, 2, ROLE, 4>(p, wsp, s);
 }
 

@@ -32,6 +32,10 @@ struct GemmParams {
     float* R; int64_t ldr;
     float qscale; int qcols;
     const int32_t* row_slot; const float* slot_scale; int slot_width; int kw;
+    // Optional LayerNorm fused after a residual epilogue (EPI_RESID with N the
+    // model width): when the launcher splits K, its row-wise reduce also writes
+    // ln_out = dt(LN(R) * ln_g + ln_b) and sets *ln_done.
+    const void* ln_g; const void* ln_b; void* ln_out; float ln_eps; bool* ln_done;
 };
 
 // Device scratch for split-K partials (fp32 [splits][M][N]); splitting is

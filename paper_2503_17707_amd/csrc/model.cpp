@@ -583,15 +583,17 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
     }
     const bool qkv_lora = use_lora && (lora_union & (PB_LORA_Q | PB_LORA_K | PB_LORA_V));
     const bool o_lora = use_lora && (lora_union & PB_LORA_O);
+    bool ln1_ready = false;  // LN1 of layer l already produced by layer l-1's fc2 reduce
     for (int l = 0; l < L; ++l) {
         HIP_TRY(hipStreamWaitEvent(s, m->ev_layer[l], 0));
         char* Aq = m->at(a.loraA) + (size_t)l * a.loraA_layer;  // [4][kw][d]
         char* Bq = m->at(a.loraB) + (size_t)l * a.loraB_layer;  // [4][d][kw]
-        {
+        if (!ln1_ready) {
             Timed t(m, PB_K_LN);
             HIP_TRY(pb::launch_layernorm(dt, x, 1, 0, m->ltensor(l, PB_T_LN1_G), m->ltensor(l, PB_T_LN1_B),
                                          u, false, N, d, c.ln_eps, s));
         }
+        ln1_ready = false;
         if (qkv_lora) {
             Timed t(m, PB_K_LORA_SHRINK);
             pb::GemmParams p{};
@@ -625,6 +627,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             p.row_slot = rowslot; p.slot_scale = sscale; p.slot_width = a.rs; p.kw = kw;
             HIP_TRY(pb::launch_gemm(dt, 4, pb::EPI_SHRINK, p, gws, s));
         }
+        bool ln2_done = false;
         {
             Timed t(m, PB_K_GEMM_O);
             pb::GemmParams p{};
@@ -635,9 +638,12 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             }
             p.bias = m->ltensor(l, PB_T_BO);
             p.R = x; p.ldr = d;
+            // LN2 rides on the split-K reduce when the launcher splits
+            p.ln_g = m->ltensor(l, PB_T_LN2_G); p.ln_b = m->ltensor(l, PB_T_LN2_B); p.ln_out = u;
+            p.ln_eps = c.ln_eps; p.ln_done = &ln2_done;
             HIP_TRY(pb::launch_gemm(dt, 1, pb::EPI_RESID, p, gws, s));
         }
-        {
+        if (!ln2_done) {
             Timed t(m, PB_K_LN);
             HIP_TRY(pb::launch_layernorm(dt, x, 1, 0, m->ltensor(l, PB_T_LN2_G), m->ltensor(l, PB_T_LN2_B),
                                          u, false, N, d, c.ln_eps, s));
@@ -656,6 +662,13 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             p.X = hbuf; p.ldx = F; p.W = m->ltensor(l, PB_T_W2); p.ldw = F; p.M = N; p.N = d; p.K1 = F;
             p.bias = m->ltensor(l, PB_T_B2);
             p.R = x; p.ldr = d;
+            // the next layer's LN1 rides on the split-K reduce when the launcher
+            // splits; its weights are read here, so wait for that layer first
+            if (l + 1 < L) {
+                HIP_TRY(hipStreamWaitEvent(s, m->ev_layer[l + 1], 0));
+                p.ln_g = m->ltensor(l + 1, PB_T_LN1_G); p.ln_b = m->ltensor(l + 1, PB_T_LN1_B);
+                p.ln_out = u; p.ln_eps = c.ln_eps; p.ln_done = &ln1_ready;
+            }
             HIP_TRY(pb::launch_gemm(dt, 3, pb::EPI_RESID, p, gws, s));
         }
     }
@@ -732,5 +745,45 @@ extern "C" int pb_prefill_first_token(pb_model* m, const int32_t* tokens, int32_
             m->tcount[k] += 1;
         }
     }
+    return PB_OK;
+}
+
+// ---- kernel-level entry points (include/pipeboost_ops.h) -------------------
+
+#include "../../include/pipeboost_ops.h"
+
+extern "C" int pb_op_gemm(int32_t dtype, int32_t epi, const void* X, const void* W, const void* bias,
+                          void* C, float* R, int32_t M, int32_t N, int32_t K, float qscale,
+                          int32_t qcols, void* workspace, size_t workspace_bytes, void* stream) {
+    if (dtype != PB_BF16 && dtype != PB_F16) return fail(PB_EINVAL, "bad dtype %d", dtype);
+    if (epi < 0 || epi > 2) return fail(PB_EINVAL, "epilogue %d not in 0..2", epi);
+    if (M < 0 || N <= 0 || K <= 0 || N % 64 || K % 64)
+        return fail(PB_EINVAL, "shape M=%d N=%d K=%d (N and K must be positive multiples of 64)", M, N, K);
+    if (!X || !W || !bias || (epi == 2 ? !R : !C)) return fail(PB_EINVAL, "NULL operand");
+    pb::GemmParams p{};
+    p.X = X; p.ldx = K; p.W = W; p.ldw = K; p.M = M; p.N = N; p.K1 = K;
+    p.bias = bias; p.C = C; p.ldc = N; p.R = R; p.ldr = N; p.qscale = qscale; p.qcols = qcols;
+    const int role = epi == 0 ? 0 : (epi == 1 ? 2 : 3);
+    const int e = epi == 0 ? pb::EPI_QKV : (epi == 1 ? pb::EPI_RELU : pb::EPI_RESID);
+    const pb::GemmWorkspace ws{workspace, workspace ? workspace_bytes : 0};
+    HIP_TRY(pb::launch_gemm(dtype, role, e, p, ws, (hipStream_t)stream));
+    return PB_OK;
+}
+
+extern "C" int pb_op_attention(int32_t dtype, const void* qkv, void* out, int32_t B, int32_t T,
+                               int32_t H, int32_t hd, void* stream) {
+    if (dtype != PB_BF16 && dtype != PB_F16) return fail(PB_EINVAL, "bad dtype %d", dtype);
+    if (B < 0 || T < 0 || H <= 0 || (hd != 64 && hd != 128)) return fail(PB_EINVAL, "bad attention shape");
+    if (!qkv || !out) return fail(PB_EINVAL, "NULL operand");
+    HIP_TRY(pb::launch_attention(dtype, qkv, out, B, T, H, hd, (hipStream_t)stream));
+    return PB_OK;
+}
+
+extern "C" int pb_op_layernorm(int32_t dtype, const float* x, const void* g, const void* b, void* out,
+                               int32_t out_f32, int32_t rows, int32_t d, float eps, void* stream) {
+    if (dtype != PB_BF16 && dtype != PB_F16) return fail(PB_EINVAL, "bad dtype %d", dtype);
+    if (rows < 0 || d <= 0 || d % 4 || d > 16384 || !(eps > 0.f)) return fail(PB_EINVAL, "bad LayerNorm shape");
+    if (!x || !g || !b || !out) return fail(PB_EINVAL, "NULL operand");
+    HIP_TRY(pb::launch_layernorm(dtype, x, 1, 0, g, b, out, out_f32 != 0, rows, d, eps, (hipStream_t)stream));
     return PB_OK;
 }
