@@ -139,7 +139,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="opt-1.3b")
     ap.add_argument("--cold-reps", type=int, default=5)
-    ap.add_argument("--oracle-layers", type=int, default=8)
+    ap.add_argument("--oracle-layers", type=int, default=0,
+                    help="layers of the CPU-oracle sample (0 = all)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (3 times) and exit: "
@@ -183,13 +184,18 @@ def main():
     toks = synth.tokens(w)
     ad = list(w.adapters())
 
-    # ---- H2D alone (the bandwidth the loader can get) -----------------------
-    m.poison(0xFF)
-    m.stream_layers(hw, w.order())
-    torch.cuda.synchronize(dev)
-    h2d_bytes, h2d_ms = m.load_stats()
-    b_meas = h2d_bytes / h2d_ms / 1e6
-    err("H2D alone: %.2f GB in %.1f ms = %.2f GB/s" % (h2d_bytes / 1e9, h2d_ms, b_meas))
+    # ---- H2D alone (the bandwidth the loader can get): copies only, median of 3
+    # after one warm-up transfer --------------------------------------------------
+    rates = []
+    for rep in range(4):
+        m.poison(0xFF)
+        m.stream_layers(hw, w.order())
+        torch.cuda.synchronize(dev)
+        h2d_bytes, h2d_ms = m.load_stats()
+        if rep:
+            rates.append(h2d_bytes / h2d_ms / 1e6)
+    b_meas = float(np.median(rates))
+    err("H2D alone: %.2f GB at %.2f GB/s (median of %d)" % (h2d_bytes / 1e9, b_meas, len(rates)))
 
     # ---- cold start: pinned host weights -> first token ---------------------
     lora_bytes = sum(b.nbytes for bl in hw.loras.values() for b in bl)
@@ -260,8 +266,9 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        err("timing the CPU oracle on %d layers ..." % args.oracle_layers)
-        cpu = oracle_baseline(w, args.oracle_layers)
+        n_or = args.oracle_layers or w.n_layers
+        err("timing the CPU oracle on %d layers ..." % n_or)
+        cpu = oracle_baseline(w, n_or)
 
     out = {
         "metric": METRIC,

@@ -274,7 +274,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmParams p, Spli
 }
 
 // Sum the split-K partials in split order, then apply the epilogue.
-template <typename T, int EPI>
+template <typename T, int EPI, int ROLE>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p, SplitArgs sa) {
     const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;  // index of a group of 4 columns
     const int64_t per_row = p.N / 4;
@@ -298,7 +298,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p, SplitA
 // ln_out[m] = dt(LN(R[m]) * g + b) with fp32 statistics.  One block per row.
 constexpr int RLN_MAXC = 16;  // float4 chunks per thread: N <= 16384
 
-template <typename T>
+template <typename T, int ROLE>
 __global__ __launch_bounds__(256) void splitk_resid_ln_kernel(GemmParams p, SplitArgs sa) {
     __shared__ float red[4];
     const int m = blockIdx.x;
@@ -385,7 +385,10 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t
     // split K when the tiles alone leave CUs idle, keeping >= PB_GEMM_MIN_KT
     // K tiles per split
     int splits = 1;
-    if (tiles < 256 && wsp.ws && wsp.bytes > 0) {
+    // (256 x 256 tiles split below 256 tiles; 128 x 128 ones only below 128,
+    // where the partial traffic costs less than the idle CUs)
+    constexpr int split_below = (BM == 128 && BN == 128) ? 128 : 256;
+    if (tiles < split_below && wsp.ws && wsp.bytes > 0) {
         splits = std::min((512 + tiles - 1) / tiles, nk1 / PB_GEMM_MIN_KT);
         const int64_t per_split = (int64_t)p.M * p.N * 4;
         splits = (int)std::min<int64_t>(splits, (int64_t)(wsp.bytes / per_split));
@@ -403,13 +406,13 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || sa.splits == 1) return e;
     if (EPI == EPI_RESID && p.ln_out && p.N <= 256 * 4 * RLN_MAXC) {
-        hipLaunchKernelGGL((splitk_resid_ln_kernel<T>), dim3(p.M), dim3(256), 0, s, p, sa);
+        hipLaunchKernelGGL((splitk_resid_ln_kernel<T, ROLE>), dim3(p.M), dim3(256), 0, s, p, sa);
         e = hipGetLastError();
         if (e == hipSuccess && p.ln_done) *p.ln_done = true;
         return e;
     }
     const int64_t groups = (int64_t)p.M * (p.N / 4);
-    hipLaunchKernelGGL((splitk_reduce_kernel<T, EPI>), dim3((unsigned)((groups + 255) / 256)), dim3(256), 0,
+    hipLaunchKernelGGL((splitk_reduce_kernel<T, EPI, ROLE>), dim3((unsigned)((groups + 255) / 256)), dim3(256), 0,
                        s, p, sa);
     return hipGetLastError();
 }
