@@ -38,6 +38,9 @@ namespace pb {
 
 namespace {
 
+#ifndef PB_GEMM_SPLIT_TARGET
+#define PB_GEMM_SPLIT_TARGET 512  // blocks a split launch aims for
+#endif
 #ifndef PB_GEMM_MIN_KT
 #define PB_GEMM_MIN_KT 8  // fewest K tiles a split-K block gets
 #endif
@@ -389,7 +392,7 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t
     // where the partial traffic costs less than the idle CUs)
     constexpr int split_below = (BM == 128 && BN == 128) ? 128 : 256;
     if (tiles < split_below && wsp.ws && wsp.bytes > 0) {
-        splits = std::min((512 + tiles - 1) / tiles, nk1 / PB_GEMM_MIN_KT);
+        splits = std::min((PB_GEMM_SPLIT_TARGET + tiles - 1) / tiles, nk1 / PB_GEMM_MIN_KT);
         const int64_t per_split = (int64_t)p.M * p.N * 4;
         splits = (int)std::min<int64_t>(splits, (int64_t)(wsp.bytes / per_split));
         if (splits < 1) splits = 1;

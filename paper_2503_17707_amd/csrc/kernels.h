@@ -66,12 +66,16 @@ hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t i
                             const void* g, const void* b, void* out, bool out_f32, int rows,
                             int d, float eps, hipStream_t s);
 
-// logits[b, v] = z[b, :] . E[v, :] (fp32 accumulate).
+// logits[b, v] = z[b, :] . E[v, :] (fp32 accumulate), plus per-block argmax
+// partials pval/pidx [B][lm_head_blocks(V)] (maximum, lowest index on ties).
+int lm_head_blocks(int V);
 hipError_t launch_lm_head(int dtype, const float* z, int B, const void* E, int V, int d,
-                          float* logits, hipStream_t s);
+                          float* logits, float* pval, int* pidx, hipStream_t s);
 
-// tok[b] = lowest index of the maximum of logits[b, :] (-1 if none is finite or ordered).
-hipError_t launch_argmax(const float* logits, int B, int V, int32_t* tok, hipStream_t s);
+// tok[b] = lowest index of the maximum of logits[b, :], from the LM head's
+// partials (-1 if no finite maximum exists).
+hipError_t launch_argmax(const float* pval, const int* pidx, int B, int V, int32_t* tok,
+                         hipStream_t s);
 
 // Scatter one adapter's staged LoRA blobs (per layer: A_t [r, d], B_t [d, r] for
 // the targets in mask) into slot `slot` of the packed per-layer arrays

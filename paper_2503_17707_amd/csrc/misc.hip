@@ -1,5 +1,7 @@
 // Memory-bound kernels of the prefill: embedding, LayerNorm, LM head, argmax
 // and the LoRA slot packing.  All read and write with 16-byte vectors.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -103,85 +105,127 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict_
     }
 }
 
-// ---- LM head: logits[b, v] = z[b] . E[v], one wave per 8 vocabulary rows ----
-constexpr int LM_ROWS = 8;
-constexpr int LM_NB = 4;  // sequences per pass
+// ---- LM head + argmax partials ----------------------------------------------
+// logits[b, v] = z[b] . E[v] for NB sequences at once; each wave takes 8
+// vocabulary rows at a time (lanes split the model width into 16-byte chunks),
+// and each block also writes, per sequence, the (max, lowest index) of the
+// rows it covered, so the final argmax only scans one partial per block.
+constexpr int LM_ROWS = 8;                      // rows per wave pass
+constexpr int LM_BLOCK_ROWS = 4 * 2 * LM_ROWS;  // 4 waves x 2 passes
 
-template <typename T>
-__global__ __launch_bounds__(256) void lm_head_kernel(const float* __restrict__ z, int B,
+__device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
+    return v > bv || (v == bv && i < bi);
+}
+
+template <typename T, int NB>
+__global__ __launch_bounds__(256) void lm_head_kernel(const float* __restrict__ z, int b0,
                                                      const T* __restrict__ E, int V, int d,
-                                                     float* __restrict__ logits) {
+                                                     float* __restrict__ logits,
+                                                     float* __restrict__ pval,
+                                                     int* __restrict__ pidx, int nblk) {
+    __shared__ float sv[4][NB];
+    __shared__ int si[4][NB];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int v0 = (blockIdx.x * 4 + wave) * LM_ROWS;
-    if (v0 >= V) return;
-    for (int b0 = 0; b0 < B; b0 += LM_NB) {
-        const int nb = min(LM_NB, B - b0);
-        float acc[LM_ROWS][LM_NB];
+    float best[NB];
+    int bidx[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        best[j] = -INFINITY;
+        bidx[j] = 0x7fffffff;
+    }
+    for (int pass = 0; pass < 2; ++pass) {
+        const int v0 = blockIdx.x * LM_BLOCK_ROWS + (pass * 4 + wave) * LM_ROWS;
+        if (v0 >= V) break;
+        float acc[LM_ROWS][NB];
 #pragma unroll
         for (int r = 0; r < LM_ROWS; ++r)
 #pragma unroll
-            for (int j = 0; j < LM_NB; ++j) acc[r][j] = 0.f;
+            for (int j = 0; j < NB; ++j) acc[r][j] = 0.f;
         for (int c = lane * 8; c < d; c += 64 * 8) {
-            float zb[LM_NB][8];
+            u32x4 ev[LM_ROWS];
 #pragma unroll
-            for (int j = 0; j < LM_NB; ++j) {
-                if (j < nb) {
-                    const f32x4 a = *(const f32x4*)(z + (int64_t)(b0 + j) * d + c);
-                    const f32x4 bq = *(const f32x4*)(z + (int64_t)(b0 + j) * d + c + 4);
+            for (int r = 0; r < LM_ROWS; ++r)
+                ev[r] = *(const u32x4*)(E + (int64_t)min(v0 + r, V - 1) * d + c);
+            float zb[NB][8];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        zb[j][e] = a[e];
-                        zb[j][4 + e] = bq[e];
-                    }
-                } else {
+            for (int j = 0; j < NB; ++j) {
+                const f32x4 a = *(const f32x4*)(z + (int64_t)(b0 + j) * d + c);
+                const f32x4 bq = *(const f32x4*)(z + (int64_t)(b0 + j) * d + c + 4);
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) zb[j][e] = 0.f;
+                for (int e = 0; e < 4; ++e) {
+                    zb[j][e] = a[e];
+                    zb[j][4 + e] = bq[e];
                 }
             }
 #pragma unroll
             for (int r = 0; r < LM_ROWS; ++r) {
-                const int v = min(v0 + r, V - 1);
-                const u32x4 ev = *(const u32x4*)(E + (int64_t)v * d + c);
                 T ea[8];
-                __builtin_memcpy(ea, &ev, 16);
+                __builtin_memcpy(ea, &ev[r], 16);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     const float w = (float)ea[e];
 #pragma unroll
-                    for (int j = 0; j < LM_NB; ++j) acc[r][j] += w * zb[j][e];
+                    for (int j = 0; j < NB; ++j) acc[r][j] += w * zb[j][e];
                 }
             }
         }
 #pragma unroll
         for (int r = 0; r < LM_ROWS; ++r)
 #pragma unroll
-            for (int j = 0; j < LM_NB; ++j) {
+            for (int j = 0; j < NB; ++j) {
                 const float t = wave_sum(acc[r][j]);
-                if (lane == 0 && j < nb && v0 + r < V) logits[(int64_t)(b0 + j) * V + v0 + r] = t;
+                const int v = v0 + r;
+                if (v < V) {
+                    if (lane == 0) logits[(int64_t)(b0 + j) * V + v] = t;
+                    if (better(t, v, best[j], bidx[j])) {
+                        best[j] = t;
+                        bidx[j] = v;
+                    }
+                }
             }
+    }
+    if (lane == 0)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            sv[wave][j] = best[j];
+            si[wave][j] = bidx[j];
+        }
+    __syncthreads();
+    if (threadIdx.x < NB) {
+        const int j = threadIdx.x;
+        float bb = sv[0][j];
+        int ii = si[0][j];
+        for (int w = 1; w < 4; ++w)
+            if (better(sv[w][j], si[w][j], bb, ii)) {
+                bb = sv[w][j];
+                ii = si[w][j];
+            }
+        pval[(int64_t)(b0 + j) * nblk + blockIdx.x] = bb;
+        pidx[(int64_t)(b0 + j) * nblk + blockIdx.x] = ii;
     }
 }
 
-// ---- argmax: one block per sequence, lowest index among equal maxima --------
-__global__ __launch_bounds__(1024) void argmax_kernel(const float* __restrict__ logits, int V,
-                                                     int32_t* __restrict__ tok) {
-    __shared__ float sv[16];
-    __shared__ int si[16];
+// ---- argmax over the per-block partials: one block per sequence ------------
+__global__ __launch_bounds__(256) void argmax_final_kernel(const float* __restrict__ pval,
+                                                          const int* __restrict__ pidx, int nblk,
+                                                          int32_t* __restrict__ tok) {
+    __shared__ float sv[4];
+    __shared__ int si[4];
     const int b = blockIdx.x;
-    const float* l = logits + (int64_t)b * V;
     float best = -INFINITY;
     int bi = 0x7fffffff;
-    for (int v = threadIdx.x; v < V; v += 1024) {
-        const float x = l[v];
-        if (x > best || (x == best && v < bi)) {
+    for (int i = threadIdx.x; i < nblk; i += 256) {
+        const float x = pval[(int64_t)b * nblk + i];
+        const int xi = pidx[(int64_t)b * nblk + i];
+        if (better(x, xi, best, bi)) {
             best = x;
-            bi = v;
+            bi = xi;
         }
     }
     for (int o = 32; o > 0; o >>= 1) {
         const float ov = __shfl_xor(best, o, 64);
         const int oi = __shfl_xor(bi, o, 64);
-        if (ov > best || (ov == best && oi < bi)) {
+        if (better(ov, oi, best, bi)) {
             best = ov;
             bi = oi;
         }
@@ -195,8 +239,8 @@ __global__ __launch_bounds__(1024) void argmax_kernel(const float* __restrict__ 
     if (threadIdx.x == 0) {
         float bb = sv[0];
         int ii = si[0];
-        for (int w = 1; w < 16; ++w)
-            if (sv[w] > bb || (sv[w] == bb && si[w] < ii)) {
+        for (int w = 1; w < 4; ++w)
+            if (better(sv[w], si[w], bb, ii)) {
                 bb = sv[w];
                 ii = si[w];
             }
@@ -267,23 +311,37 @@ hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t i
     return hipGetLastError();
 }
 
+int lm_head_blocks(int V) { return (V + LM_BLOCK_ROWS - 1) / LM_BLOCK_ROWS; }
+
 hipError_t launch_lm_head(int dtype, const float* z, int B, const void* E, int V, int d,
-                          float* logits, hipStream_t s) {
+                          float* logits, float* pval, int* pidx, hipStream_t s) {
     if (B <= 0 || V <= 0) return hipSuccess;
     if (d % 8) return hipErrorInvalidValue;
-    const int blocks = (V + 4 * LM_ROWS - 1) / (4 * LM_ROWS);
-    if (dtype == 1)
-        hipLaunchKernelGGL(lm_head_kernel<_Float16>, dim3(blocks), dim3(256), 0, s, z, B,
-                           (const _Float16*)E, V, d, logits);
-    else
-        hipLaunchKernelGGL(lm_head_kernel<__bf16>, dim3(blocks), dim3(256), 0, s, z, B,
-                           (const __bf16*)E, V, d, logits);
-    return hipGetLastError();
+    const int blocks = lm_head_blocks(V);
+    for (int b0 = 0; b0 < B; b0 += 4) {
+        const int nb = std::min(4, B - b0);
+#define PB_LM(T, NB)                                                                           \
+    hipLaunchKernelGGL((lm_head_kernel<T, NB>), dim3(blocks), dim3(256), 0, s, z, b0,          \
+                       (const T*)E, V, d, logits, pval, pidx, blocks)
+        if (dtype == 1) {
+            if (nb == 1) PB_LM(_Float16, 1); else if (nb == 2) PB_LM(_Float16, 2);
+            else if (nb == 3) PB_LM(_Float16, 3); else PB_LM(_Float16, 4);
+        } else {
+            if (nb == 1) PB_LM(__bf16, 1); else if (nb == 2) PB_LM(__bf16, 2);
+            else if (nb == 3) PB_LM(__bf16, 3); else PB_LM(__bf16, 4);
+        }
+#undef PB_LM
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
-hipError_t launch_argmax(const float* logits, int B, int V, int32_t* tok, hipStream_t s) {
+hipError_t launch_argmax(const float* pval, const int* pidx, int B, int V, int32_t* tok,
+                         hipStream_t s) {
     if (B <= 0) return hipSuccess;
-    hipLaunchKernelGGL(argmax_kernel, dim3(B), dim3(1024), 0, s, logits, V, tok);
+    hipLaunchKernelGGL(argmax_final_kernel, dim3(B), dim3(256), 0, s, pval, pidx,
+                       lm_head_blocks(V), tok);
     return hipGetLastError();
 }
 

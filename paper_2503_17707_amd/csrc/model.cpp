@@ -150,6 +150,7 @@ struct ArenaLayout {
     int rs, kw;  // LoRA slot width (rank rounded up to 8) and packed width (multiple of 64)
     size_t globals, layers, layer_bytes, loraA, loraB, loraA_layer, loraB_layer;
     size_t x, u, qkv, attn, h, z, rowslot, tokens, slotscale, zf, logits, outtok, staging, ws;
+    size_t pval, pidx;
     size_t staging_bytes, total;
 };
 
@@ -185,6 +186,8 @@ ArenaLayout arena_layout(const pb_config* c) {
     a.zf = take(B * d * 4);
     a.logits = take(B * V * 4);
     a.outtok = take(B * 4);
+    a.pval = take(B * (size_t)pb::lm_head_blocks((int)V) * 4);
+    a.pidx = take(B * (size_t)pb::lm_head_blocks((int)V) * 4);
     a.staging_bytes = c->max_adapters > 0 ? L * lora_layer_elems(c, c->max_rank, 0xF) * 2 : 0;
     a.staging = take(a.staging_bytes);
     a.ws = take(GEMM_WS_BYTES);
@@ -681,11 +684,12 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
     {
         Timed t(m, PB_K_LM_HEAD);
         HIP_TRY(pb::launch_lm_head(dt, zf, B, m->gtensor(PB_G_EMBED), c.vocab, d,
-                                   (float*)m->at(a.logits), s));
+                                   (float*)m->at(a.logits), (float*)m->at(a.pval), (int*)m->at(a.pidx), s));
     }
     {
         Timed t(m, PB_K_ARGMAX);
-        HIP_TRY(pb::launch_argmax((const float*)m->at(a.logits), B, c.vocab, (int32_t*)m->at(a.outtok), s));
+        HIP_TRY(pb::launch_argmax((const float*)m->at(a.pval), (const int*)m->at(a.pidx), B, c.vocab,
+                                  (int32_t*)m->at(a.outtok), s));
     }
     return PB_OK;
 }
