@@ -369,7 +369,13 @@ __global__ __launch_bounds__(256) void splitk_resid_ln_kernel(GemmParams p, Spli
 #pragma unroll
             for (int r = 0; r < 4; ++r) y[r] = (v[i][r] - mean) * rstd * (float)ga[r] + (float)ba[r];
             *(u32x2*)((T*)p.ln_out + (int64_t)m * p.N + 4 * c) = pack4<T>(y[0], y[1], y[2], y[3]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[i][r] = (float)(T)y[r];  // u as it enters the GEMM
         }
+    }
+    if (p.shrink.Acat) {
+        __shared__ float red16[4][16];
+        row_shrink<T, RLN_MAXC>(p.shrink, m, p.N, v, red16);
     }
 }
 

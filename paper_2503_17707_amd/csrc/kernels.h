@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "rowops.h"
+
 namespace pb {
 
 enum GemmEpilogue {
@@ -36,6 +38,8 @@ struct GemmParams {
     // model width): when the launcher splits K, its row-wise reduce also writes
     // ln_out = dt(LN(R) * ln_g + ln_b) and sets *ln_done.
     const void* ln_g; const void* ln_b; void* ln_out; float ln_eps; bool* ln_done;
+    // Optional LoRA shrink of the fused LayerNorm's rows (Acat NULL = none).
+    RowShrink shrink;
 };
 
 // Device scratch for split-K partials (fp32 [splits][M][N]); splitting is
@@ -62,9 +66,10 @@ hipError_t launch_embed(int dtype, const int32_t* tok, const void* E, const void
 
 // out[r, :] = LN(x[r * in_mul + in_add, :]) * g + b, fp32 statistics;
 // out_f32 selects a float output, otherwise dt.
+// With sh (dt output only), also writes the row-wise LoRA shrink of each row.
 hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t in_add,
                             const void* g, const void* b, void* out, bool out_f32, int rows,
-                            int d, float eps, hipStream_t s);
+                            int d, float eps, hipStream_t s, const RowShrink* sh = nullptr);
 
 // logits[b, v] = z[b, :] . E[v, :] (fp32 accumulate), plus per-block argmax
 // partials pval/pidx [B][lm_head_blocks(V)] (maximum, lowest index on ties).

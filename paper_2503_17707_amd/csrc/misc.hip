@@ -54,7 +54,7 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict_
                                                        int64_t in_mul, int64_t in_add,
                                                        const T* __restrict__ g,
                                                        const T* __restrict__ b, void* out,
-                                                       int d, float eps) {
+                                                       int d, float eps, RowShrink sh) {
     __shared__ float red[4];
     const int row = blockIdx.x;
     const float* xr = x + ((int64_t)row * in_mul + in_add) * d;
@@ -100,8 +100,14 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict_
                 *(f32x4*)((float*)out + (int64_t)row * d + 4 * c) = f32x4{y[0], y[1], y[2], y[3]};
             } else {
                 *(u32x2*)((T*)out + (int64_t)row * d + 4 * c) = pack4<T>(y[0], y[1], y[2], y[3]);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[i][r] = (float)(T)y[r];  // u as it enters the GEMM
             }
         }
+    }
+    if (!OUT_F32 && sh.Acat) {
+        __shared__ float red16[4][16];
+        row_shrink<T, LN_MAXC>(sh, row, d, v, red16);
     }
 }
 
@@ -296,12 +302,14 @@ hipError_t launch_embed(int dtype, const int32_t* tok, const void* E, const void
 
 hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t in_add,
                             const void* g, const void* b, void* out, bool out_f32, int rows,
-                            int d, float eps, hipStream_t s) {
+                            int d, float eps, hipStream_t s, const RowShrink* shp) {
     if (rows <= 0) return hipSuccess;
     if (d % 4 || d > 256 * 4 * LN_MAXC) return hipErrorInvalidValue;
+    RowShrink sh{};
+    if (shp && !out_f32) sh = *shp;
 #define PB_LN(T, F)                                                                            \
     hipLaunchKernelGGL((layernorm_kernel<T, F>), dim3(rows), dim3(256), 0, s, x, in_mul, in_add, \
-                       (const T*)g, (const T*)b, out, d, eps)
+                       (const T*)g, (const T*)b, out, d, eps, sh)
     if (dtype == 1) {
         if (out_f32) PB_LN(_Float16, true); else PB_LN(_Float16, false);
     } else {

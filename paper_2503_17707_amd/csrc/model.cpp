@@ -52,6 +52,7 @@ constexpr int MAX_SLOTS = 16;
 constexpr int MAX_RANK = 64;
 constexpr size_t VEC_ALIGN = 128;  // elements (256 bytes of dt)
 constexpr size_t GEMM_WS_BYTES = 64u << 20;  // split-K partials
+constexpr int ROW_SHRINK_MAX_TOKENS = 1024;     // fuse the q/k/v LoRA shrink up to this many tokens
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -586,18 +587,31 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
     }
     const bool qkv_lora = use_lora && (lora_union & (PB_LORA_Q | PB_LORA_K | PB_LORA_V));
     const bool o_lora = use_lora && (lora_union & PB_LORA_O);
-    bool ln1_ready = false;  // LN1 of layer l already produced by layer l-1's fc2 reduce
+    // For few tokens the q/k/v LoRA shrink rides on the kernel that writes the
+    // LayerNorm rows (row-wise dot products); for many it is a GEMM.
+    const bool fuse_shrink = qkv_lora && N <= ROW_SHRINK_MAX_TOKENS;
+    auto row_shrink_args = [&](int layer) {
+        pb::RowShrink sh{};
+        if (fuse_shrink) {
+            sh.Acat = m->at(a.loraA) + (size_t)layer * a.loraA_layer;
+            sh.row_slot = rowslot; sh.slot_scale = sscale; sh.Z = z;
+            sh.rs = a.rs; sh.kw = kw; sh.mask = lora_union & 7u;
+        }
+        return sh;
+    };
+    bool ln1_ready = false;  // LN1 (and its fused shrink) of layer l produced by layer l-1's fc2 reduce
     for (int l = 0; l < L; ++l) {
         HIP_TRY(hipStreamWaitEvent(s, m->ev_layer[l], 0));
         char* Aq = m->at(a.loraA) + (size_t)l * a.loraA_layer;  // [4][kw][d]
         char* Bq = m->at(a.loraB) + (size_t)l * a.loraB_layer;  // [4][d][kw]
         if (!ln1_ready) {
             Timed t(m, PB_K_LN);
+            const pb::RowShrink sh = row_shrink_args(l);
             HIP_TRY(pb::launch_layernorm(dt, x, 1, 0, m->ltensor(l, PB_T_LN1_G), m->ltensor(l, PB_T_LN1_B),
-                                         u, false, N, d, c.ln_eps, s));
+                                         u, false, N, d, c.ln_eps, s, &sh));
         }
         ln1_ready = false;
-        if (qkv_lora) {
+        if (qkv_lora && !fuse_shrink) {
             Timed t(m, PB_K_LORA_SHRINK);
             pb::GemmParams p{};
             p.X = u; p.ldx = d; p.W = Aq; p.ldw = d; p.M = N; p.N = 3 * kw; p.K1 = d;
@@ -671,6 +685,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
                 HIP_TRY(hipStreamWaitEvent(s, m->ev_layer[l + 1], 0));
                 p.ln_g = m->ltensor(l + 1, PB_T_LN1_G); p.ln_b = m->ltensor(l + 1, PB_T_LN1_B);
                 p.ln_out = u; p.ln_eps = c.ln_eps; p.ln_done = &ln1_ready;
+                p.shrink = row_shrink_args(l + 1);
             }
             HIP_TRY(pb::launch_gemm(dt, 3, pb::EPI_RESID, p, gws, s));
         }

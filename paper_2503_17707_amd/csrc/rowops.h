@@ -1,0 +1,114 @@
+// Row-wise LoRA shrink fused into the kernels that produce a LayerNorm row.
+//
+// For token m with adapter slot s >= 0, and each target t in {q, k, v} of the
+// mask, Z[m, t*kw + s*rs + j] = dt(scale_s * sum_k u[m, k] * Acat[t][s*rs + j][k])
+// for j < rs (ranks past the adapter's own are zero rows of Acat), and every
+// other column of Z[m, 0 .. 3 kw) is 0, exactly the layout the shrink GEMM
+// writes.  u enters rounded to dt, as it enters the projection GEMM.
+#pragma once
+
+#include "common.h"
+
+namespace pb {
+
+struct RowShrink {
+    const void* Acat;        // this layer's [4][kw][d] A slots (dt); NULL = no shrink
+    const int32_t* row_slot; // [M]
+    const float* slot_scale; // [16]
+    void* Z;                 // [M][4 kw] (dt)
+    int rs, kw;
+    uint32_t mask;           // targets q=1, k=2, v=4
+};
+
+// Sum of each of 16 per-lane values over the 64 lanes of a wave, by halving
+// exchanges: afterwards lane l holds the total of value index
+// 8 b5 + 4 b4 + 2 b3 + b2 (b_k = bit k of l).  17 exchanges instead of 96.
+__device__ __forceinline__ float wave_sum16(const float (&p)[16], int lane) {
+    const bool h5 = (lane >> 5) & 1, h4 = (lane >> 4) & 1, h3 = (lane >> 3) & 1, h2 = (lane >> 2) & 1;
+    float a8[8], a4[4], a2[2];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const float send = h5 ? p[k] : p[8 + k];
+        a8[k] = (h5 ? p[8 + k] : p[k]) + __shfl_xor(send, 32, 64);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const float send = h4 ? a8[k] : a8[4 + k];
+        a4[k] = (h4 ? a8[4 + k] : a8[k]) + __shfl_xor(send, 16, 64);
+    }
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const float send = h3 ? a4[k] : a4[2 + k];
+        a2[k] = (h3 ? a4[2 + k] : a4[k]) + __shfl_xor(send, 8, 64);
+    }
+    float a1 = (h2 ? a2[1] : a2[0]) + __shfl_xor(h2 ? a2[0] : a2[1], 4, 64);
+    a1 += __shfl_xor(a1, 2, 64);
+    a1 += __shfl_xor(a1, 1, 64);
+    return a1;
+}
+
+// u: this thread's values of the row, chunk i covers columns 4 (tid + 256 i) .. +3
+// (chunks past the row's end may hold anything).  Must be called by all 256
+// threads of the block (it synchronizes).  The loads of a chunk's 16 A rows
+// are unconditional (ranks past rs re-read row rs - 1 and are dropped) so that
+// they are in flight together.
+template <typename T, int MAXC>
+__device__ __forceinline__ void row_shrink(const RowShrink& sh, int m, int d, const f32x4 (&u)[MAXC],
+                                           float (*red)[16]) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nc = d / 4;
+    const int slot = sh.row_slot[m];
+    T* zr = (T*)sh.Z + (int64_t)m * 4 * sh.kw;
+    // zero every column outside the row's own slot block of an active target
+    for (int c = tid; c < 3 * sh.kw; c += 256) {
+        const int t = c / sh.kw, cc = c % sh.kw;
+        const bool own = slot >= 0 && ((sh.mask >> t) & 1u) && cc >= slot * sh.rs && cc < (slot + 1) * sh.rs;
+        if (!own) zr[c] = (T)0.f;
+    }
+    if (slot < 0) return;  // uniform across the block
+    const float scale = sh.slot_scale[slot];
+    const T* A = (const T*)sh.Acat;
+    const int o_lane = 8 * ((lane >> 5) & 1) + 4 * ((lane >> 4) & 1) + 2 * ((lane >> 3) & 1) + ((lane >> 2) & 1);
+    for (int t = 0; t < 3; ++t) {
+        if (!((sh.mask >> t) & 1u)) continue;
+        for (int j0 = 0; j0 < sh.rs; j0 += 16) {
+            const T* rows[16];
+#pragma unroll
+            for (int o = 0; o < 16; ++o)
+                rows[o] = A + (int64_t)(t * sh.kw + slot * sh.rs + min(j0 + o, sh.rs - 1)) * d;
+            float part[16];
+#pragma unroll
+            for (int o = 0; o < 16; ++o) part[o] = 0.f;
+#pragma unroll
+            for (int i = 0; i < MAXC; ++i) {
+                if (256 * i >= nc) break;  // uniform
+                const int c = tid + 256 * i;
+                const bool valid = c < nc;
+                const int cc = valid ? c : 0;
+                u32x2 raw[16];
+#pragma unroll
+                for (int o = 0; o < 16; ++o) raw[o] = *(const u32x2*)(rows[o] + 4 * cc);
+                float uu[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) uu[r] = valid ? u[i][r] : 0.f;
+#pragma unroll
+                for (int o = 0; o < 16; ++o) {
+                    T a4[4];
+                    __builtin_memcpy(a4, &raw[o], 8);
+                    part[o] += uu[0] * (float)a4[0] + uu[1] * (float)a4[1] + uu[2] * (float)a4[2] +
+                               uu[3] * (float)a4[3];
+                }
+            }
+            const float tot = wave_sum16(part, lane);
+            __syncthreads();  // previous use of red finished
+            if ((lane & 3) == 0) red[wave][o_lane] = tot;
+            __syncthreads();
+            if (tid < 16 && j0 + tid < sh.rs) {
+                const float zsum = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
+                zr[t * sh.kw + slot * sh.rs + j0 + tid] = (T)(scale * zsum);
+            }
+        }
+    }
+}
+
+}  // namespace pb
