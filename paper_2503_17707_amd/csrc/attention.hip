@@ -33,25 +33,6 @@ namespace {
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr int BKV = 64;  // keys per tile
 
-// One 16-byte global -> LDS copy per lane (LDS-DMA): lane i writes bytes
-// [16 i, 16 i + 16) after the wave-uniform LDS address lds_base.  M0 is saved
-// and restored; waiting is left to the explicit s_waitcnt below.
-__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
-    uint32_t saved;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\t"
-        "s_mov_b32 m0, %1\n\t"
-        "global_load_lds_dwordx4 %2, off\n\t"
-        "s_mov_b32 m0, %0"
-        : "=&s"(saved)
-        : "s"(lds_base), "v"(gptr)
-        : "memory");
-}
-
-__device__ __forceinline__ void wait_vmcnt0() {
-    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
-}
-
 // 16-byte chunk permutations of a K or V tile row (key = row): K is read as
 // 16 consecutive rows at one chunk, V by transposing 8-byte reads of four
 // consecutive rows at two neighbouring chunks.
@@ -141,7 +122,7 @@ void attention_kernel(const T* __restrict__ qkv,
     const int nkb = min((T_len + BKV - 1) / BKV, ((qb + 1) * BQ + BKV - 1) / BKV);
     issue(0, 0);
     for (int kb = 0; kb < nkb; ++kb) {
-        wait_vmcnt0();
+        wait_vmcnt<0>();
         __syncthreads();  // tile kb visible; stage of tile kb-1 free
         if (kb + 1 < nkb) issue(kb + 1, (kb + 1) & 1);
         const uint8_t* sK = smem + (kb & 1) * STAGE;

@@ -6,11 +6,15 @@
 // four consecutive output features of one token: the epilogue writes 8-byte
 // (dt) or 16-byte (fp32 residual) vectors.
 //
-// Block tile BM x BN, K tile 64: 256 x 256 or 128 x 128 with 8 waves (2 x 4,
-// two waves per SIMD, chosen by how many tiles the shape gives), and 64 x 64
-// with 4 waves for the LoRA shrink and for N not a multiple of 128.  Tiles go straight from
-// global memory into an S-stage LDS ring (LDS-DMA, no staging registers), so
-// S-1 tiles are in flight while one is multiplied; one barrier per K tile.
+// Block tile BM x BN, K tile 64: 256 x 256 (2-stage ring, 128 KiB of LDS) or
+// 128 x 128 (3-stage ring: with few tiles the weights arrive cold from HBM
+// and a deeper ring hides more of that latency) with 8 waves (2 x 4, two waves
+// per SIMD), chosen by how many tiles the shape gives, and 64 x 64 with 4
+// waves for N not a multiple of 128.  Tiles go straight from global memory
+// into the S-stage LDS ring (LDS-DMA, no staging registers), so S-1 tiles are
+// in flight while one is multiplied; one barrier per K tile.  The operand
+// reads from LDS, not the MFMA rate, bound the smaller tiles: a wave's
+// WM x WN sub-tile reads (WM + WN) rows per K tile.
 // LDS rows are 128 bytes (64 elements) with the 16-byte chunks XOR-swizzled by
 // the row index so that the MFMA operand reads of 16 consecutive rows are free
 // of bank conflicts (the DMA writes the swizzle by choosing which chunk each
@@ -39,10 +43,22 @@ namespace pb {
 namespace {
 
 #ifndef PB_GEMM_SPLIT_TARGET
-#define PB_GEMM_SPLIT_TARGET 512  // blocks a split launch aims for
+#define PB_GEMM_SPLIT_TARGET 256  // blocks a split launch aims for
 #endif
 #ifndef PB_GEMM_MIN_KT
 #define PB_GEMM_MIN_KT 8  // fewest K tiles a split-K block gets
+#endif
+#ifndef PB_GEMM_S128
+#define PB_GEMM_S128 3  // LDS ring depth of the 128 x 128 tiles
+#endif
+#ifndef PB_GEMM_S64
+#define PB_GEMM_S64 4  // ... of the 64 x 64 tiles
+#endif
+#ifndef PB_GEMM_T64
+#define PB_GEMM_T64 0  // 64 x 64 tiles over full K where 128 x 128 ones would need a K split
+#endif
+#ifndef PB_GEMM_S256
+#define PB_GEMM_S256 2  // ... of the 256 x 256 tiles
 #endif
 
 constexpr int BK = 64;
@@ -99,33 +115,6 @@ struct SplitArgs {
     float* ws;      // [splits][M][N] fp32 partials when splits > 1
 };
 
-// One 16-byte global -> LDS copy per lane (LDS-DMA, global_load_lds_dwordx4):
-// lane i writes bytes [16 i, 16 i + 16) after the wave-uniform LDS address
-// lds_base.  Issued from inline assembly so that the compiler, which would
-// otherwise drain every outstanding load before the next LDS read, leaves the
-// waiting to the explicit s_waitcnt of the pipeline below; later
-// compiler-placed waits only ever wait for more, never less.
-// M0 is saved and restored around the copy, so the compiler's own use of M0
-// is never disturbed.
-__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
-    uint32_t saved;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\t"
-        "s_mov_b32 m0, %1\n\t"
-        "global_load_lds_dwordx4 %2, off\n\t"
-        "s_mov_b32 m0, %0"
-        : "=&s"(saved)
-        : "s"(lds_base), "v"(gptr)
-        : "memory");
-}
-
-// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
 template <typename T, int EPI, int BM, int BN, int WGM, int WGN, int ROLE, int S>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmParams p, SplitArgs sa) {
     typedef typename Mfma<T>::vec8 vec8;
@@ -177,24 +166,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmParams p, Spli
     // DMA instruction j of this wave fills LDS rows 8g .. 8g+7, g = wave + NW j;
     // rows < BM hold X (tokens), the rest W (output features): slots j < NLX.
     // Lane i writes row 8g + i/8, physical chunk i%8, which holds logical K
-    // chunk (i%8) ^ (row & 7).  Element offsets fit in 31 bits (checked by the
-    // launcher); off1 addresses the base operands, off2 the LoRA ones.
+    // chunk (i%8) ^ (row & 7) = (i%8) ^ (i/8) for every j.  Rows past the
+    // matrix edge re-read its last row.  Element offsets fit in 31 bits
+    // (checked by the launcher); they are recomputed per tile rather than
+    // held in registers.
     const int lrow = lane >> 3;
-    int off1[NL], off2[NL];
-#pragma unroll
-    for (int j = 0; j < NL; ++j) {
-        const int row = 8 * (wave + NW * j) + lrow;
-        const int ch = swz(row, lane & 7);
-        if (j < NLX) {
-            const int m = min(m0 + row, p.M - 1);
-            off1[j] = m * (int)p.ldx + ch * 8;
-            off2[j] = m * (int)p.ldx2 + ch * 8;
-        } else {
-            const int n = min(n0 + row - BM, p.N - 1);
-            off1[j] = n * (int)p.ldw + ch * 8;
-            off2[j] = n * (int)p.ldw2 + ch * 8;
-        }
-    }
+    const int chk = swz(lrow, lane & 7) * 8;
+    const int xr0 = m0 + 8 * wave + lrow, wr0 = n0 + 8 * wave + lrow - BM;
     const T* Xb = (const T*)p.X;
     const T* Wb = (const T*)p.W;
     const T* W2 = (const T*)p.W2;
@@ -204,10 +182,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmParams p, Spli
         const bool base = t < nk1;
         const T* xp = base ? Xb : X2;
         const T* wp = base ? Wb : W2;
-        const int k = (base ? t : t - nk1) * BK;
+        const int ldx = base ? (int)p.ldx : (int)p.ldx2;
+        const int ldw = base ? (int)p.ldw : (int)p.ldw2;
+        const int k = (base ? t : t - nk1) * BK + chk;
 #pragma unroll
         for (int j = 0; j < NL; ++j) {
-            const int off = (base ? off1[j] : off2[j]) + k;
+            const int off = j < NLX ? min(xr0 + 8 * NW * j, p.M - 1) * ldx + k
+                                    : min(wr0 + 8 * NW * j, p.N - 1) * ldw + k;
             dma16((j < NLX ? xp : wp) + off,
                   sbase + (uint32_t)__builtin_amdgcn_readfirstlane((wave + NW * j) * 1024));
         }
@@ -432,9 +413,10 @@ hipError_t launch_tiles(const GemmParams& p, const GemmWorkspace& wsp, hipStream
     // 256 x 256 when those tiles fill the GPU, or half fill it over a long K
     // (then split along K); else 128 x 128 (split along K when too few)
     if (p.N % 256 == 0 && (tiles(256, 256) >= 256 || (tiles(256, 256) >= 128 && p.K1 >= 8192)))
-        return launch_cfg<T, EPI, 256, 256, 2, 4, ROLE, 2>(p, wsp, s);
-    if (p.N % 128 == 0) return launch_cfg<T, EPI, 128, 128, 2, 4, ROLE, 2>(p, wsp, s);
-    return launch_cfg<T, EPI, 64, 64, 2, 2, ROLE, 4>(p, wsp, s);
+        return launch_cfg<T, EPI, 256, 256, 2, 4, ROLE, PB_GEMM_S256>(p, wsp, s);
+    const bool small64 = PB_GEMM_T64 && tiles(128, 128) < 128 && tiles(64, 64) >= 256;
+    if (p.N % 128 == 0 && !small64) return launch_cfg<T, EPI, 128, 128, 2, 4, ROLE, PB_GEMM_S128>(p, wsp, s);
+    return launch_cfg<T, EPI, 64, 64, 2, 2, ROLE, PB_GEMM_S64>(p, wsp, s);
 }
 
 template <typename T>
