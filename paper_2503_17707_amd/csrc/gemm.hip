@@ -279,10 +279,13 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p, SplitA
 
 // Row-wise split-K reduce of a residual projection fused with the LayerNorm
 // that follows it: R[m] += (sum of partials in split order) + bias, then
-// ln_out[m] = dt(LN(R[m]) * g + b) with fp32 statistics.  One block per row.
-constexpr int RLN_MAXC = 16;  // float4 chunks per thread: N <= 16384
+// ln_out[m] = dt(LN(R[m]) * g + b) with fp32 statistics, and optionally the
+// row's LoRA shrink.  One block per row; MAXC float4 chunks per thread (N <=
+// 1024 MAXC); NS splits known at compile time (0: any count, summed in a loop)
+// so that every partial of a chunk is in flight at once.
+constexpr int RLN_MAXC = 16;  // largest chunk count: N <= 16384
 
-template <typename T, int ROLE>
+template <typename T, int ROLE, int MAXC, int NS>
 __global__ __launch_bounds__(256) void splitk_resid_ln_kernel(GemmParams p, SplitArgs sa) {
     __shared__ float red[4];
     const int m = blockIdx.x;
@@ -290,24 +293,27 @@ __global__ __launch_bounds__(256) void splitk_resid_ln_kernel(GemmParams p, Spli
     const int64_t stride = (int64_t)p.M * p.N;
     float* xr = p.R + (int64_t)m * p.ldr;
     const float* wr = sa.ws + (int64_t)m * p.N;
-    f32x4 v[RLN_MAXC];
+    f32x4 v[MAXC];
     float sum = 0.f;
 #pragma unroll
-    for (int i = 0; i < RLN_MAXC; ++i) {
+    for (int i = 0; i < MAXC; ++i) {
         const int c = threadIdx.x + 256 * i;
         if (c < nc) {
-            f32x4 a = *(const f32x4*)(wr + 4 * c);
-            for (int s = 1; s < sa.splits; ++s) {
-                const f32x4 w = *(const f32x4*)(wr + s * stride + 4 * c);
-                a[0] += w[0];
-                a[1] += w[1];
-                a[2] += w[2];
-                a[3] += w[3];
-            }
+            f32x4 w[NS > 0 ? NS : 1];
+#pragma unroll
+            for (int s = 0; s < (NS > 0 ? NS : 1); ++s) w[s] = *(const f32x4*)(wr + s * stride + 4 * c);
             const u32x2 braw = *(const u32x2*)((const T*)p.bias + 4 * c);
+            f32x4 x = *(const f32x4*)(xr + 4 * c);
+            f32x4 a = w[0];
+#pragma unroll
+            for (int s = 1; s < NS; ++s) a = f32x4{a[0] + w[s][0], a[1] + w[s][1], a[2] + w[s][2], a[3] + w[s][3]};
+            if (NS == 0)
+                for (int s = 1; s < sa.splits; ++s) {
+                    const f32x4 u = *(const f32x4*)(wr + s * stride + 4 * c);
+                    a = f32x4{a[0] + u[0], a[1] + u[1], a[2] + u[2], a[3] + u[3]};
+                }
             T bb[4];
             __builtin_memcpy(bb, &braw, 8);
-            f32x4 x = *(const f32x4*)(xr + 4 * c);
 #pragma unroll
             for (int r = 0; r < 4; ++r) x[r] += a[r] + (float)bb[r];
             *(f32x4*)(xr + 4 * c) = x;
@@ -315,49 +321,35 @@ __global__ __launch_bounds__(256) void splitk_resid_ln_kernel(GemmParams p, Spli
             sum += (x[0] + x[1]) + (x[2] + x[3]);
         }
     }
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    sum = wave_sum(sum);
-    if (lane == 0) red[wave] = sum;
-    __syncthreads();
-    const float mean = (red[0] + red[1] + red[2] + red[3]) / (float)p.N;
-    __syncthreads();
-    float q = 0.f;
-#pragma unroll
-    for (int i = 0; i < RLN_MAXC; ++i) {
-        const int c = threadIdx.x + 256 * i;
-        if (c < nc)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float t = v[i][r] - mean;
-                q += t * t;
-            }
-    }
-    q = wave_sum(q);
-    if (lane == 0) red[wave] = q;
-    __syncthreads();
-    const float var = (red[0] + red[1] + red[2] + red[3]) / (float)p.N;
-    const float rstd = 1.0f / sqrtf(var + p.ln_eps);
-#pragma unroll
-    for (int i = 0; i < RLN_MAXC; ++i) {
-        const int c = threadIdx.x + 256 * i;
-        if (c < nc) {
-            const u32x2 graw = *(const u32x2*)((const T*)p.ln_g + 4 * c);
-            const u32x2 braw = *(const u32x2*)((const T*)p.ln_b + 4 * c);
-            T ga[4], ba[4];
-            __builtin_memcpy(ga, &graw, 8);
-            __builtin_memcpy(ba, &braw, 8);
-            float y[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) y[r] = (v[i][r] - mean) * rstd * (float)ga[r] + (float)ba[r];
-            *(u32x2*)((T*)p.ln_out + (int64_t)m * p.N + 4 * c) = pack4<T>(y[0], y[1], y[2], y[3]);
-#pragma unroll
-            for (int r = 0; r < 4; ++r) v[i][r] = (float)(T)y[r];  // u as it enters the GEMM
-        }
-    }
+    row_layernorm<T, MAXC, false>(v, sum, nc, (const T*)p.ln_g, (const T*)p.ln_b,
+                                  (T*)p.ln_out + (int64_t)m * p.N, p.ln_eps, red);
     if (p.shrink.Acat) {
         __shared__ float red16[4][16];
-        row_shrink<T, RLN_MAXC>(p.shrink, m, p.N, v, red16);
+        row_shrink<T, MAXC>(p.shrink, m, p.N, v, red16);
     }
+}
+
+template <typename T, int ROLE>
+hipError_t launch_resid_ln(const GemmParams& p, const SplitArgs& sa, hipStream_t s) {
+#define PB_RLN(MAXC, NS) \
+    hipLaunchKernelGGL((splitk_resid_ln_kernel<T, ROLE, MAXC, NS>), dim3(p.M), dim3(256), 0, s, p, sa)
+    // few rows (latency-bound): every partial in flight at once; many rows:
+    // occupancy hides the latency and registers matter more
+    if (p.N <= 2048) {
+        if (sa.splits == 2) PB_RLN(2, 2);
+        else if (sa.splits == 4) PB_RLN(2, 4);
+        else PB_RLN(2, 0);
+    } else if (p.N <= 4096) {
+        if (sa.splits == 2) PB_RLN(4, 2);
+        else if (sa.splits == 4) PB_RLN(4, 4);
+        else PB_RLN(4, 0);
+    } else if (p.N <= 8192) {
+        PB_RLN(8, 0);
+    } else {
+        PB_RLN(RLN_MAXC, 0);
+    }
+#undef PB_RLN
+    return hipGetLastError();
 }
 
 template <typename T, int EPI, int BM, int BN, int WGM, int WGN, int ROLE, int S>
@@ -396,8 +388,7 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || sa.splits == 1) return e;
     if (EPI == EPI_RESID && p.ln_out && p.N <= 256 * 4 * RLN_MAXC) {
-        hipLaunchKernelGGL((splitk_resid_ln_kernel<T, ROLE>), dim3(p.M), dim3(256), 0, s, p, sa);
-        e = hipGetLastError();
+        e = launch_resid_ln<T, ROLE>(p, sa, s);
         if (e == hipSuccess && p.ln_done) *p.ln_done = true;
         return e;
     }

@@ -40,16 +40,7 @@ __global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ 
 // ---- LayerNorm: one 256-thread block per row, values kept in registers ------
 constexpr int LN_MAXC = 16;  // float4 chunks per thread: d <= 256 * 4 * 16
 
-__device__ __forceinline__ float block_sum(float v, float* red) {
-    v = wave_sum(v);
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    __syncthreads();
-    if (lane == 0) red[wave] = v;
-    __syncthreads();
-    return red[0] + red[1] + red[2] + red[3];
-}
-
-template <typename T, bool OUT_F32>
+template <typename T, bool OUT_F32, int MAXC>
 __global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict__ x,
                                                        int64_t in_mul, int64_t in_add,
                                                        const T* __restrict__ g,
@@ -59,55 +50,21 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict_
     const int row = blockIdx.x;
     const float* xr = x + ((int64_t)row * in_mul + in_add) * d;
     const int nc = d / 4;
-    f32x4 v[LN_MAXC];
+    f32x4 v[MAXC];
     float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < LN_MAXC; ++i) {
+    for (int i = 0; i < MAXC; ++i) {
         const int c = threadIdx.x + 256 * i;
         if (c < nc) {
             v[i] = *(const f32x4*)(xr + 4 * c);
             s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
         }
     }
-    const float mean = block_sum(s, red) / (float)d;
-    float q = 0.f;
-#pragma unroll
-    for (int i = 0; i < LN_MAXC; ++i) {
-        const int c = threadIdx.x + 256 * i;
-        if (c < nc) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float t = v[i][r] - mean;
-                q += t * t;
-            }
-        }
-    }
-    const float var = block_sum(q, red) / (float)d;
-    const float rstd = 1.0f / sqrtf(var + eps);
-#pragma unroll
-    for (int i = 0; i < LN_MAXC; ++i) {
-        const int c = threadIdx.x + 256 * i;
-        if (c < nc) {
-            const u32x2 graw = *(const u32x2*)(g + 4 * c);
-            const u32x2 braw = *(const u32x2*)(b + 4 * c);
-            T ga[4], ba[4];
-            __builtin_memcpy(ga, &graw, 8);
-            __builtin_memcpy(ba, &braw, 8);
-            float y[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) y[r] = (v[i][r] - mean) * rstd * (float)ga[r] + (float)ba[r];
-            if (OUT_F32) {
-                *(f32x4*)((float*)out + (int64_t)row * d + 4 * c) = f32x4{y[0], y[1], y[2], y[3]};
-            } else {
-                *(u32x2*)((T*)out + (int64_t)row * d + 4 * c) = pack4<T>(y[0], y[1], y[2], y[3]);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) v[i][r] = (float)(T)y[r];  // u as it enters the GEMM
-            }
-        }
-    }
+    void* orow = OUT_F32 ? (void*)((float*)out + (int64_t)row * d) : (void*)((T*)out + (int64_t)row * d);
+    row_layernorm<T, MAXC, OUT_F32>(v, s, nc, g, b, orow, eps, red);
     if (!OUT_F32 && sh.Acat) {
         __shared__ float red16[4][16];
-        row_shrink<T, LN_MAXC>(sh, row, d, v, red16);
+        row_shrink<T, MAXC>(sh, row, d, v, red16);
     }
 }
 
@@ -307,15 +264,23 @@ hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t i
     if (d % 4 || d > 256 * 4 * LN_MAXC) return hipErrorInvalidValue;
     RowShrink sh{};
     if (shp && !out_f32) sh = *shp;
-#define PB_LN(T, F)                                                                            \
-    hipLaunchKernelGGL((layernorm_kernel<T, F>), dim3(rows), dim3(256), 0, s, x, in_mul, in_add, \
+#define PB_LN1(T, F, C)                                                                            \
+    hipLaunchKernelGGL((layernorm_kernel<T, F, C>), dim3(rows), dim3(256), 0, s, x, in_mul, in_add, \
                        (const T*)g, (const T*)b, out, d, eps, sh)
+#define PB_LN(T, F)                                                                                \
+    do {                                                                                           \
+        if (d <= 2048) PB_LN1(T, F, 2);                                                            \
+        else if (d <= 4096) PB_LN1(T, F, 4);                                                       \
+        else if (d <= 8192) PB_LN1(T, F, 8);                                                       \
+        else PB_LN1(T, F, LN_MAXC);                                                                \
+    } while (0)
     if (dtype == 1) {
         if (out_f32) PB_LN(_Float16, true); else PB_LN(_Float16, false);
     } else {
         if (out_f32) PB_LN(__bf16, true); else PB_LN(__bf16, false);
     }
 #undef PB_LN
+#undef PB_LN1
     return hipGetLastError();
 }
 

@@ -20,6 +20,69 @@ struct RowShrink {
     uint32_t mask;           // targets q=1, k=2, v=4
 };
 
+// Sum over the 256 threads of a block (4 waves); red holds 4 floats.
+__device__ __forceinline__ float block_sum256(float v, float* red) {
+    v = wave_sum(v);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    __syncthreads();  // previous use of red finished
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// LayerNorm of one row of d = 4 nc values held by the 256 threads of a block
+// as float4 chunks (chunk i of a thread = columns 4 (tid + 256 i) .. +3; sum =
+// this thread's sum of its values): out = LN(v) * g + b with fp32 statistics
+// (biased variance), written as dt, or fp32 when OUT_F32.  g and b are loaded
+// before the reductions so that their latency hides behind them.  For dt
+// output v is left holding the values rounded to dt, as the next GEMM reads them.
+template <typename T, int MAXC, bool OUT_F32>
+__device__ __forceinline__ void row_layernorm(f32x4 (&v)[MAXC], float sum, int nc, const T* g, const T* b,
+                                              void* out_row, float eps, float* red) {
+    const int tid = threadIdx.x;
+    u32x2 graw[MAXC], braw[MAXC];
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i) {
+        const int c = tid + 256 * i;
+        if (c < nc) {
+            graw[i] = *(const u32x2*)(g + 4 * c);
+            braw[i] = *(const u32x2*)(b + 4 * c);
+        }
+    }
+    const float inv_d = 1.0f / (float)(4 * nc);
+    const float mean = block_sum256(sum, red) * inv_d;
+    float q = 0.f;
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i)
+        if (tid + 256 * i < nc)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float t = v[i][r] - mean;
+                q += t * t;
+            }
+    const float var = block_sum256(q, red) * inv_d;
+    const float rstd = 1.0f / sqrtf(var + eps);
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i) {
+        const int c = tid + 256 * i;
+        if (c < nc) {
+            T ga[4], ba[4];
+            __builtin_memcpy(ga, &graw[i], 8);
+            __builtin_memcpy(ba, &braw[i], 8);
+            float y[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) y[r] = (v[i][r] - mean) * rstd * (float)ga[r] + (float)ba[r];
+            if (OUT_F32) {
+                *(f32x4*)((float*)out_row + 4 * c) = f32x4{y[0], y[1], y[2], y[3]};
+            } else {
+                *(u32x2*)((T*)out_row + 4 * c) = pack4<T>(y[0], y[1], y[2], y[3]);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[i][r] = (float)(T)y[r];
+            }
+        }
+    }
+}
+
 // Sum of each of 16 per-lane values over the 64 lanes of a wave, by halving
 // exchanges: afterwards lane l holds the total of value index
 // 8 b5 + 4 b4 + 2 b3 + b2 (b_k = bit k of l).  17 exchanges instead of 96.
