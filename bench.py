@@ -132,6 +132,54 @@ def oracle_baseline(w, n_layers):
                                                              w.seq_len)}
 
 
+def h2d_sweep(w, pb, torch, np):
+    """Best sustained pinned host -> device rate: the loader over the workload's
+    layer blobs at several chunk sizes, and plain pinned copies of 1 MiB .. 1 GiB
+    on one and on two streams (median of 3 after a warm-up)."""
+    cfg = pb.make_config(w)
+    hw = pb.HostWeights(w, cfg)
+    m = pb.Model(cfg, "cuda:0")
+    loader = {}
+    for mib in (1, 4, 16, 64, 256, 1024):
+        m.set_chunk_bytes(mib << 20)
+        rates = []
+        for rep in range(4):
+            m.stream_layers(hw, w.order())
+            torch.cuda.synchronize()
+            b, ms = m.load_stats()
+            if rep:
+                rates.append(b / ms / 1e6)
+        loader[str(mib)] = float(np.median(rates))
+    m.set_chunk_bytes(256 << 20)
+    m.destroy()
+    hw.free()
+    plain = {}
+    for mib in (1, 4, 16, 64, 256, 1024):
+        n = mib << 20
+        reps = max(1, (2 << 30) // n)  # about 2 GiB per timing
+        for ns in (1, 2):
+            srcs = [torch.empty(n, dtype=torch.uint8, pin_memory=True) for _ in range(ns)]
+            dsts = [torch.empty(n, dtype=torch.uint8, device="cuda:0") for _ in range(ns)]
+            streams = [torch.cuda.Stream() for _ in range(ns)]
+            rates = []
+            for rep in range(4):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                for i in range(reps):
+                    with torch.cuda.stream(streams[i % ns]):
+                        dsts[i % ns].copy_(srcs[i % ns], non_blocking=True)
+                torch.cuda.synchronize()
+                if rep:
+                    rates.append(n * reps / (time.perf_counter() - t0) / 1e9)
+            plain["%d MiB x %d stream%s" % (mib, ns, "s" if ns > 1 else "")] = float(np.median(rates))
+            del srcs, dsts
+    best = max(list(loader.values()) + list(plain.values()))
+    return {"h2d_sweep": {"workload": w.name, "loader_GBps_by_chunk_MiB": loader,
+                          "plain_pinned_copy_GBps": plain, "best_GBps": best,
+                          "pcie_gen5_x16_GBps": PCIE5_X16_GBPS,
+                          "best_frac_of_pcie": best / PCIE5_X16_GBPS}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -145,6 +193,9 @@ def main():
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (3 times) and exit: "
                          "the reference kernel for scaling HBM byte counters")
+    ap.add_argument("--h2d-sweep", action="store_true",
+                    help="only measure the loader's H2D rate over chunk sizes, and plain pinned "
+                         "copies on one and two streams, then exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -170,6 +221,9 @@ def main():
 
     pb.lib()  # fails loudly if the HIP library is missing
     w = synth.WORKLOADS[args.workload]
+    if args.h2d_sweep:
+        print(json.dumps(h2d_sweep(w, pb, torch, np)), flush=True)
+        return
     dev = torch.device("cuda:0")
     t0 = time.perf_counter()
     cfg = pb.make_config(w)
@@ -296,6 +350,9 @@ def main():
                        "h2d_GBps_during_cold_start": float(np.median(loads)),
                        "h2d_GBps_alone": b_meas, "pcie_gen5_x16_GBps": PCIE5_X16_GBPS,
                        "bound_ms": bound_ms, "frac_of_bound": bound_ms / ttft_med,
+                       "bound_terms_ms": {"h2d_bytes_over_B_meas": bound_ms,
+                                          "flops_over_warm_rate": ms_step},
+                       "ttft_over_max_bound": ttft_med / max(bound_ms, ms_step),
                        "init_ms": init_ms},
         "h2d": {"GBps": b_meas, "frac_of_pcie_gen5_x16": b_meas / PCIE5_X16_GBPS},
         "roofline": roofline,

@@ -1,0 +1,144 @@
+"""Summaries of rocprofv3 CSV output for the cold-start path (markdown on stdout).
+
+  python -m paper_2503_17707_amd.profsum overlap DIR LABEL
+      DIR from `rocprofv3 --kernel-trace --memory-copy-trace -f csv -d DIR -o ov
+      -- python bench.py ...`: for every cold start in the run (a burst of
+      host-to-device copies followed by the library's kernels), how much of the
+      compute ran while weights were still being copied, and the compute tail
+      left after the last copy.
+
+  python -m paper_2503_17707_amd.profsum mfma DIR LABEL
+      DIR from `rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_F16 SQ_VALU_MFMA_BUSY_CYCLES
+      SQ_BUSY_CU_CYCLES GRBM_GUI_ACTIVE -f csv -d DIR -o mf -- python bench.py ...`:
+      per kernel, the MFMA work executed and the fraction of SIMD cycles the
+      matrix units were busy.
+
+Only reads files; used to write the summaries kept with the profiles.
+"""
+import collections
+import csv
+import glob
+import os
+import re
+import sys
+
+N_XCD = 8           # GRBM_GUI_ACTIVE is summed over the 8 XCDs
+N_SIMD = 256 * 4    # SQ_VALU_MFMA_BUSY_CYCLES is summed over every SIMD
+GAP_NS = 350_000  # copies further apart than this start a new load (within a load: < 0.25 ms)
+
+
+def _one(d, pattern):
+    files = glob.glob(os.path.join(d, pattern))
+    if len(files) != 1:
+        raise SystemExit("expected one %s in %s, found %d" % (pattern, d, len(files)))
+    return files[0]
+
+
+def kind_of(name):
+    """Kernel family of a mangled kernel name (GEMM role from its template arguments)."""
+    roles = {0: "gemm_qkv", 1: "gemm_o", 2: "gemm_fc1", 3: "gemm_fc2", 4: "lora_shrink"}
+    m = re.search(r"gemm_kernelIDF16b?_((?:Li\d+E)+)", name) or \
+        re.search(r"gemm_kernelIDF16_((?:Li\d+E)+)", name)
+    if m:
+        a = [int(x) for x in re.findall(r"Li(\d+)E", m.group(1))]
+        return roles.get(a[5], "gemm")
+    if "splitk_resid_ln_kernel" in name:
+        return roles[int(re.search(r"splitk_resid_ln_kernelIDF16b?_Li(\d+)E", name).group(1))] + " reduce"
+    if "splitk_reduce_kernel" in name:
+        return roles[int(re.search(r"splitk_reduce_kernelIDF16b?_Li\d+ELi(\d+)E", name).group(1))] + " reduce"
+    for k in ("attention", "layernorm", "lm_head", "argmax", "embed", "lora_pack"):
+        if k in name:
+            return k
+    return None
+
+
+def _union(iv):
+    out = []
+    for s, e in sorted(iv):
+        if out and s <= out[-1][1]:
+            out[-1][1] = max(out[-1][1], e)
+        else:
+            out.append([s, e])
+    return out
+
+
+def _inter(u, lo, hi):
+    return sum(max(0, min(e, hi) - max(s, lo)) for s, e in u)
+
+
+def overlap(d, label):
+    copies = [(int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
+              for r in csv.DictReader(open(_one(d, "*memory_copy_trace.csv")))
+              if r["Direction"].endswith("HOST_TO_DEVICE")]
+    kernels = [(int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"])
+               for r in csv.DictReader(open(_one(d, "*kernel_trace.csv")))]
+    copies.sort()
+    loads = []
+    for s, e in copies:
+        if loads and s - loads[-1][1] < GAP_NS:
+            loads[-1][1] = max(loads[-1][1], e)
+            loads[-1][2] += 1
+        else:
+            loads.append([s, e, 1])
+    rows = []
+    for i, (cs, ce, n) in enumerate(loads):
+        nxt = loads[i + 1][0] if i + 1 < len(loads) else float("inf")
+        ends = [e for s, e, name in kernels if cs <= s < nxt and kind_of(name) == "argmax"]
+        if not ends:
+            continue  # a load with no prefill behind it (bandwidth measurement)
+        end = min(ends)  # the first prefill after the load ends at its argmax
+        ks = [(s, e) for s, e, name in kernels if cs <= s and e <= end and kind_of(name)]
+        u = _union(ks)
+        busy = sum(e - s for s, e in u)
+        rows.append((n, (ce - cs) / 1e6, busy / 1e6, _inter(u, cs, ce) / max(busy, 1),
+                     max(0, end - ce) / 1e6, (end - cs) / 1e6))
+    out = ["# Copy / compute overlap during cold starts, %s\n" % label,
+           "Each row is one cold start of the run (the first is the warm-up): host-to-device "
+           "copies of the layer stream and the LoRA staging, then the prefill, whose kernels "
+           "each wait for their layer's copy event.  Overlap = share of the prefill's kernel "
+           "busy time that falls inside the copy window; tail = time from the last copy's end "
+           "to the argmax's end.\n",
+           "| cold start | copies | copy window ms | kernel busy ms | overlap | tail ms | "
+           "first copy -> argmax ms |", "|---|---|---|---|---|---|---|"]
+    for i, (n, win, busy, ov, tail, span) in enumerate(rows):
+        out.append("| %d%s | %d | %.2f | %.2f | %.3f | %.2f | %.2f |" % (
+            i, " (warm-up)" if i == 0 else "", n, win, busy, ov, tail, span))
+    return "\n".join(out)
+
+
+def mfma(d, label):
+    per = collections.defaultdict(lambda: collections.defaultdict(list))
+    for r in csv.DictReader(open(_one(d, "*counter_collection.csv"))):
+        k = kind_of(r["Kernel_Name"])
+        if k:
+            per[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    out = ["# MFMA work and matrix-unit busy fraction per kernel kind, %s\n" % label,
+           "Counters per dispatch, averaged over the run's dispatches of each kind.  MFMA "
+           "FLOPs = SQ_INSTS_VALU_MFMA_MOPS_F16 x 512.  Busy = SQ_VALU_MFMA_BUSY_CYCLES / "
+           "(GRBM_GUI_ACTIVE / %d XCDs x %d SIMDs): the share of all SIMD cycles, over the "
+           "dispatch, in which the matrix unit was busy.  Counter runs serialize dispatches, so "
+           "launch gaps are absent here.\n" % (N_XCD, N_SIMD),
+           "| kind | dispatches | MFMA GFLOP per dispatch | GPU cycles per dispatch | "
+           "MFMA busy |", "|---|---|---|---|---|"]
+    for k in sorted(per):
+        c = per[k]
+        if not c.get("GRBM_GUI_ACTIVE"):
+            continue
+        n = len(c["GRBM_GUI_ACTIVE"])
+        mops = sum(c.get("SQ_INSTS_VALU_MFMA_MOPS_F16", [0])) / n
+        busy = sum(c.get("SQ_VALU_MFMA_BUSY_CYCLES", [0])) / n
+        gui = sum(c["GRBM_GUI_ACTIVE"]) / n / N_XCD
+        out.append("| %s | %d | %.3f | %.0f | %.3f |" % (k, n, mops * 512 / 1e9, gui,
+                                                          busy / (gui * N_SIMD) if gui else 0.0))
+    return "\n".join(out)
+
+
+def main(argv):
+    if len(argv) != 3 or argv[0] not in ("overlap", "mfma"):
+        raise SystemExit(__doc__)
+    fn = overlap if argv[0] == "overlap" else mfma
+    print(fn(argv[1], argv[2]))
+
+
+if __name__ == "__main__":
+    main(sys.argv[1:])
