@@ -37,7 +37,15 @@ constexpr int BKV = 64;  // keys per tile
 // 16 consecutive rows at one chunk, V by transposing 8-byte reads of four
 // consecutive rows at two neighbouring chunks.
 __device__ __forceinline__ int kswz(int row, int ch) { return ch ^ (row & 7); }
-__device__ __forceinline__ int vswz(int row, int ch) { return ch ^ ((row & 3) << 1); }
+template <int HD>
+__device__ __forceinline__ int vswz(int row, int ch) {
+    // rows 4 g + j (j = 0..3) of one transposing read land in distinct banks
+    // by (row & 3); bit 2 of the row moves rows 4..7 off the banks of rows
+    // 0..3 (to the other half of a 256-byte row, or to the other chunk pairs
+    // of a 128-byte one): half the bank conflicts of (row & 3) alone, measured
+    if (HD == 128) return ch ^ ((row & 3) << 1) ^ (((row >> 2) & 1) << 3);
+    return ch ^ (((row & 3) ^ ((row >> 2) & 1)) << 1);
+}
 
 // Transposing LDS read (ds_read_b64_tr_b16): within each group of 16 lanes,
 // lane i receives element i % 4 of the 8-byte segments addressed by lanes
@@ -101,7 +109,7 @@ void attention_kernel(const T* __restrict__ qkv,
             const bool isv = I >= NI / 2;
             const int row = RPI * (I % (NI / 2)) + lane / CPR;
             const int pch = lane % CPR;
-            const int ch = isv ? vswz(row, pch) : kswz(row, pch);
+            const int ch = isv ? vswz<HD>(row, pch) : kswz(row, pch);
             const int key = min(kb * BKV + row, T_len - 1);
             const T* src = qkv + (row0 + key) * ld + (isv ? 2 * d : d) + h * HD + ch * 8;
             dma16(src, sbase + (uint32_t)__builtin_amdgcn_readfirstlane(I * 1024));
@@ -144,8 +152,8 @@ void attention_kernel(const T* __restrict__ qkv,
                 for (int cs = 0; cs < CS; ++cs) sc[qg][jt] = Mfma<T>::mma(kf[cs], qf[qg][cs], sc[qg][jt]);
             }
         }
-        // online softmax per query (fp32); P rounded to dt as it enters the MFMA,
-        // and the running sum adds the rounded values
+        // online softmax per query (fp32); P is rounded to dt as it enters the
+        // MFMA, the running sum adds the fp32 values
         const bool edge = ((kb + 1) * BKV > q0) || ((kb + 1) * BKV > T_len);
         vec8 pf[NQG][2];
 #pragma unroll
@@ -169,9 +177,12 @@ void attention_kernel(const T* __restrict__ qkv,
             mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
             mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
             // key kb*64 <= q_idx always holds for a computed tile, so m_new is finite
-            const float m_new = fmaxf(m_run[qg], mx);
-            // arguments are <= 0: the hardware exp2 (v_exp_f32) is exact enough and
-            // maps -inf to 0
+            // The running max is kept unless the tile exceeds it by more than
+            // 8 in log2 units, so P stays below 2^8 (well inside dt) and the
+            // accumulators are rescaled only when some query's max moved.
+            const float m_new = mx * LOG2E > m_run[qg] * LOG2E + 8.f ? fmaxf(m_run[qg], mx) : m_run[qg];
+            // arguments are <= 0 (<= 8 with the lazy max): the hardware exp2
+            // (v_exp_f32) is exact enough and maps -inf to 0
             const float alpha = __builtin_amdgcn_exp2f((m_run[qg] - m_new) * LOG2E);
             const float mb = m_new * LOG2E;
             T pt[4][4];
@@ -180,20 +191,22 @@ void attention_kernel(const T* __restrict__ qkv,
             for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const T pv = (T)__builtin_amdgcn_exp2f(sc[qg][jt][r] * LOG2E - mb);
-                    pt[jt][r] = pv;
-                    psum += (float)pv;
+                    const float e = __builtin_amdgcn_exp2f(sc[qg][jt][r] * LOG2E - mb);
+                    pt[jt][r] = (T)e;
+                    psum += e;
                 }
             psum += __shfl_xor(psum, 16, 64);
             psum += __shfl_xor(psum, 32, 64);
             l_run[qg] = l_run[qg] * alpha + psum;
             m_run[qg] = m_new;
+            if (__any(alpha != 1.f)) {
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct) {
-                o[qg][ct][0] *= alpha;
-                o[qg][ct][1] *= alpha;
-                o[qg][ct][2] *= alpha;
-                o[qg][ct][3] *= alpha;
+                for (int ct = 0; ct < CT; ++ct) {
+                    o[qg][ct][0] *= alpha;
+                    o[qg][ct][1] *= alpha;
+                    o[qg][ct][2] *= alpha;
+                    o[qg][ct][3] *= alpha;
+                }
             }
             // P^T operand of key step ks: k index 8 lg + 4 hh + r <-> key 32 ks + 16 hh + 4 lg + r
 #pragma unroll
@@ -223,7 +236,7 @@ void attention_kernel(const T* __restrict__ qkv,
                     const int row = 32 * ks + 16 * hh + 4 * lg + tj;
                     const int col = 16 * ct + 4 * tq;  // element column
                     const int ch = col >> 3;
-                    v[hh] = read_tr16<T>(sV + row * RB + (vswz(row, ch) << 4) + (col & 7) * 2);
+                    v[hh] = read_tr16<T>(sV + row * RB + (vswz<HD>(row, ch) << 4) + (col & 7) * 2);
                 }
                 const vec8 vf = as_vec8<T>(u32x4{v[0][0], v[0][1], v[1][0], v[1][1]});
 #pragma unroll

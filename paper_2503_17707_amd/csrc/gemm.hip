@@ -115,6 +115,70 @@ struct SplitArgs {
     float* ws;      // [splits][M][N] fp32 partials when splits > 1
 };
 
+// Which output tile and K range a block works on: the hardware deals
+// consecutive blocks round-robin to the 8 XCDs, so the block id is remapped to
+// give each XCD a contiguous run; runs are split-major, and tiles are walked in
+// groups of GROUP_M tile-rows so that blocks sharing an XCD's L2 share rows of
+// X and of W.  Split s takes base K tiles [s kt, (s+1) kt), the last split
+// also the LoRA K tiles of its output group (if that group is active).
+struct TileJob {
+    int m0, n0, split, nk1, t_begin, nk;
+    const void* X2;  // LoRA activations of the tile's output group
+};
+
+template <int BM, int BN>
+__device__ __forceinline__ TileJob tile_job(const GemmParams& p, const SplitArgs& sa) {
+    const int tiles_m = (p.M + BM - 1) / BM;
+    const int tiles_n = (p.N + BN - 1) / BN;
+    const int tiles = tiles_m * tiles_n;
+    int bid = blockIdx.x;
+    const int nblk = gridDim.x;
+    if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
+    const int tile = bid % tiles, split = bid / tiles;
+    const int per_group = GROUP_M * tiles_n;
+    const int first_m = (tile / per_group) * GROUP_M;
+    const int gsize = min(tiles_m - first_m, GROUP_M);
+    TileJob j;
+    j.m0 = (first_m + (tile % per_group) % gsize) * BM;
+    j.n0 = ((tile % per_group) / gsize) * BN;
+    j.split = split;
+    j.nk1 = p.K1 / BK;
+    int nk2 = 0;
+    j.X2 = p.X2;
+    if (p.K2 > 0) {
+        const int g = j.n0 / p.group;
+        if ((p.k2_mask >> g) & 1u) {
+            nk2 = p.K2 / BK;
+            j.X2 = (const char*)p.X2 + (int64_t)g * p.x2_group_stride * 2;
+        }
+    }
+    j.t_begin = split * sa.kt_split;
+    const int t_end = (split == sa.splits - 1) ? j.nk1 + nk2 : min(j.nk1, j.t_begin + sa.kt_split);
+    j.nk = t_end - j.t_begin;
+    return j;
+}
+
+// Epilogue of a wave's accumulators: acc[i][j] holds output features
+// nb + 16 i + 4 lg + r (r = 0..3) of token mb + 16 j + lr.
+template <typename T, int EPI, int MF, int NF>
+__device__ __forceinline__ void store_tile(const GemmParams& p, const SplitArgs& sa, int split, int mb, int nb,
+                                           int lr, int lg, const f32x4 (&acc)[NF][MF]) {
+#pragma unroll
+    for (int j = 0; j < MF; ++j) {
+        const int m = mb + j * 16 + lr;
+        if (m >= p.M) continue;
+#pragma unroll
+        for (int i = 0; i < NF; ++i) {
+            const int n = nb + i * 16 + 4 * lg;
+            if (n >= p.N) continue;
+            if (sa.splits > 1)
+                *(f32x4*)(sa.ws + ((int64_t)split * p.M + m) * p.N + n) = acc[i][j];
+            else
+                epilogue4<T, EPI>(p, m, n, acc[i][j]);
+        }
+    }
+}
+
 template <typename T, int EPI, int BM, int BN, int WGM, int WGN, int ROLE, int S>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmParams p, SplitArgs sa) {
     typedef typename Mfma<T>::vec8 vec8;
@@ -131,37 +195,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmParams p, Spli
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WGM, wn = wave / WGM;
-    const int tiles_m = (p.M + BM - 1) / BM;
-    const int tiles_n = (p.N + BN - 1) / BN;
-    const int tiles = tiles_m * tiles_n;
-
-    // XCD-contiguous block order, then split, then grouped tile order
-    int bid = blockIdx.x;
-    const int nblk = gridDim.x;
-    if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
-    const int tile = bid % tiles, split = bid / tiles;
-    const int per_group = GROUP_M * tiles_n;
-    const int gid = tile / per_group;
-    const int first_m = gid * GROUP_M;
-    const int gsize = min(tiles_m - first_m, GROUP_M);
-    const int tm = first_m + (tile % per_group) % gsize;
-    const int tn = (tile % per_group) / gsize;
-    const int m0 = tm * BM, n0 = tn * BN;
-
-    const int nk1 = p.K1 / BK;
-    int nk2 = 0;
-    const T* X2 = (const T*)p.X2;
-    if (p.K2 > 0) {
-        const int g = n0 / p.group;
-        if ((p.k2_mask >> g) & 1u) {
-            nk2 = p.K2 / BK;
-            X2 += (int64_t)g * p.x2_group_stride;
-        }
-    }
-    // K-tile range of this split
-    const int t_begin = split * sa.kt_split;
-    const int t_end = (split == sa.splits - 1) ? nk1 + nk2 : min(nk1, t_begin + sa.kt_split);
-    const int nk = t_end - t_begin;
+    const TileJob jb = tile_job<BM, BN>(p, sa);
+    const int m0 = jb.m0, n0 = jb.n0, split = jb.split, nk1 = jb.nk1, t_begin = jb.t_begin, nk = jb.nk;
+    const T* X2 = (const T*)jb.X2;
 
     // DMA instruction j of this wave fills LDS rows 8g .. 8g+7, g = wave + NW j;
     // rows < BM hold X (tokens), the rest W (output features): slots j < NLX.
@@ -240,21 +276,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmParams p, Spli
         compute(t % S);
     }
 
-    // epilogue: lane holds n = nb + 4*lg + r (r = 0..3) of token m
-#pragma unroll
-    for (int j = 0; j < MF; ++j) {
-        const int m = m0 + wm * WM + j * 16 + lr;
-        if (m >= p.M) continue;
-#pragma unroll
-        for (int i = 0; i < NF; ++i) {
-            const int n = n0 + wn * WN + i * 16 + 4 * lg;
-            if (n >= p.N) continue;
-            if (sa.splits > 1)
-                *(f32x4*)(sa.ws + ((int64_t)split * p.M + m) * p.N + n) = acc[i][j];
-            else
-                epilogue4<T, EPI>(p, m, n, acc[i][j]);
-        }
-    }
+    store_tile<T, EPI, MF, NF>(p, sa, split, m0 + wm * WM, n0 + wn * WN, lr, lg, acc);
 }
 
 // Sum the split-K partials in split order, then apply the epilogue.
@@ -352,23 +374,14 @@ hipError_t launch_resid_ln(const GemmParams& p, const SplitArgs& sa, hipStream_t
     return hipGetLastError();
 }
 
-template <typename T, int EPI, int BM, int BN, int WGM, int WGN, int ROLE, int S>
-hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t s) {
-    constexpr int LDS = S * (BM + BN) * ROW_BYTES;
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<T, EPI, BM, BN, WGM, WGN, ROLE, S>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
-        if (e != hipSuccess) return e;
-        attr_set = true;
-    }
-    const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
+// K split of a launch: split when the tiles alone leave CUs idle, aiming at
+// PB_GEMM_SPLIT_TARGET blocks and keeping >= PB_GEMM_MIN_KT K tiles per split
+// (256 x 256 tiles split below 256 tiles; 128 x 128 ones only below 128,
+// where the partial traffic costs less than the idle CUs).
+template <int BM, int BN>
+SplitArgs plan_split(const GemmParams& p, const GemmWorkspace& wsp, int tiles) {
     const int nk1 = p.K1 / BK;
-    // split K when the tiles alone leave CUs idle, keeping >= PB_GEMM_MIN_KT
-    // K tiles per split
     int splits = 1;
-    // (256 x 256 tiles split below 256 tiles; 128 x 128 ones only below 128,
-    // where the partial traffic costs less than the idle CUs)
     constexpr int split_below = (BM == 128 && BN == 128) ? 128 : 256;
     if (tiles < split_below && wsp.ws && wsp.bytes > 0) {
         splits = std::min((PB_GEMM_SPLIT_TARGET + tiles - 1) / tiles, nk1 / PB_GEMM_MIN_KT);
@@ -382,13 +395,15 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t
     // the LoRA tiles); S = ceil(nk1 / kt_split) leaves no split empty
     sa.splits = (nk1 + sa.kt_split - 1) / sa.kt_split;
     sa.ws = (float*)wsp.ws;
-    hipLaunchKernelGGL((gemm_kernel<T, EPI, BM, BN, WGM, WGN, ROLE, S>), dim3(tiles * sa.splits),
-                       dim3(64 * WGM * WGN), LDS, s,
-                       p, sa);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || sa.splits == 1) return e;
+    return sa;
+}
+
+// After a split launch: the row-wise reduce (fused with the residual and the
+// following LayerNorm where the caller asks for it).
+template <typename T, int EPI, int ROLE>
+hipError_t finish_split(const GemmParams& p, const SplitArgs& sa, hipStream_t s) {
     if (EPI == EPI_RESID && p.ln_out && p.N <= 256 * 4 * RLN_MAXC) {
-        e = launch_resid_ln<T, ROLE>(p, sa, s);
+        const hipError_t e = launch_resid_ln<T, ROLE>(p, sa, s);
         if (e == hipSuccess && p.ln_done) *p.ln_done = true;
         return e;
     }
@@ -396,6 +411,25 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t
     hipLaunchKernelGGL((splitk_reduce_kernel<T, EPI, ROLE>), dim3((unsigned)((groups + 255) / 256)), dim3(256), 0,
                        s, p, sa);
     return hipGetLastError();
+}
+
+template <typename T, int EPI, int BM, int BN, int WGM, int WGN, int ROLE, int S>
+hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t s) {
+    constexpr int LDS = S * (BM + BN) * ROW_BYTES;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<T, EPI, BM, BN, WGM, WGN, ROLE, S>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
+    const SplitArgs sa = plan_split<BM, BN>(p, wsp, tiles);
+    hipLaunchKernelGGL((gemm_kernel<T, EPI, BM, BN, WGM, WGN, ROLE, S>), dim3(tiles * sa.splits),
+                       dim3(64 * WGM * WGN), LDS, s, p, sa);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess || sa.splits == 1) return e;
+    return finish_split<T, EPI, ROLE>(p, sa, s);
 }
 
 template <typename T, int EPI, int ROLE>
