@@ -113,8 +113,9 @@ size_t pb_arena_bytes(const pb_config* cfg);
 
 /* ---- pinned host memory ------------------------------------------------ */
 
-/* Allocate / free pinned host memory (hipHostMalloc).  The loader accepts
- * only pinned host blobs, so that every copy is a DMA from locked pages. */
+/* Allocate / free pinned host memory (hipHostMalloc).  Layer blobs in pinned
+ * memory are copied by DMA straight from their pages; LoRA blobs must be
+ * pinned. */
 int pb_host_alloc(size_t bytes, void** out);
 int pb_host_free(void* ptr);
 
@@ -133,12 +134,20 @@ int pb_model_create(const pb_config* cfg, void* dev_arena, size_t arena_bytes, v
  * layer_order[0], layer_order[1], ..., each split into chunks of at most the
  * model's chunk size (pb_set_chunk_bytes), and records one event after each
  * layer's last chunk.  host_layers[l] is layer l's blob (indexed by layer id,
- * not by position in the order); host_globals is the globals blob.  All must
- * be pinned (PB_ENOTPINNED otherwise) and stay valid and unmodified until the
- * next pb_prefill_first_token returns.  layer_order must be a permutation of
- * 0..n_layers-1 (PB_EINVAL otherwise).  Returns immediately: the copies are
- * asynchronous.  The layer each position lands in does not depend on the
- * order, and neither do the results of a later prefill. */
+ * not by position in the order); host_globals is the globals blob.  They stay
+ * valid and unmodified until the next pb_prefill_first_token returns.
+ * layer_order must be a permutation of 0..n_layers-1 and no blob NULL
+ * (PB_EINVAL otherwise).  Blobs in pinned memory are copied by DMA from their
+ * own pages.  If any blob is pageable (hosts may cap locked memory below the
+ * model's size), the library copies pageable blobs through its own pinned
+ * staging ring (4 x 64 MiB, allocated on first use; PB_ENOMEM if it cannot
+ * be) with multi-threaded host copies, on a loader thread that enqueues every
+ * blob in the same order; pb_prefill_first_token then waits on the host until
+ * each layer's copies are enqueued before it enqueues the wait for that
+ * layer.  Returns immediately: the copies are asynchronous.  The layer each
+ * position lands in does not depend on the order, and neither do the results
+ * of a later prefill.  Errors of the loader thread surface from the next
+ * pb_prefill_first_token or pb_last_load_stats. */
 int pb_stream_layers(pb_model* m, const int32_t* layer_order, int32_t n_layers,
                      const void* const* host_layers, const void* host_globals);
 

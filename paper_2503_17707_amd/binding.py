@@ -187,13 +187,40 @@ class Pinned:
             pass
 
 
-class HostWeights:
-    """Pinned host blobs of a workload in the library's device layout, drawn by synth."""
+class Pageable:
+    """A page-aligned ordinary (pageable) host buffer with the interface of Pinned."""
 
-    def __init__(self, w, cfg: Config):
+    def __init__(self, nbytes: int):
+        self._buf = np.empty(nbytes + 4096, np.uint8)
+        off = (-self._buf.ctypes.data) % 4096
+        self._arr = self._buf[off:off + nbytes]
+        self.ptr = self._arr.ctypes.data
+        self.nbytes = nbytes
+
+    def view(self, dtype=np.uint8) -> np.ndarray:
+        return self._arr.view(dtype)
+
+    def free(self):
+        self._buf = self._arr = None
+        self.ptr = None
+
+
+# Host memory the layer blobs may pin (the rest stay pageable and the loader
+# stages them through its own pinned ring): hosts can cap locked memory well
+# below their RAM.  PIPEBOOST_PIN_BUDGET_GB overrides.
+DEFAULT_PIN_BUDGET = int(float(os.environ.get("PIPEBOOST_PIN_BUDGET_GB", "48")) * (1 << 30))
+
+
+class HostWeights:
+    """Host blobs of a workload in the library's device layout, drawn by synth:
+    the globals and LoRA blobs pinned, layer blobs pinned while they fit in
+    pin_budget bytes (in layer-id order) and pageable after that."""
+
+    def __init__(self, w, cfg: Config, pin_budget: Optional[int] = None):
         import synth
 
         self.w, self.cfg = w, cfg
+        budget = DEFAULT_PIN_BUDGET if pin_budget is None else pin_budget
         L = lib()
         kind = w.dtype
         self.layer_bytes = L.pb_layer_bytes(ctypes.byref(cfg))
@@ -206,8 +233,13 @@ class HostWeights:
             off, _ = globals_tensor(cfg, name)
             synth.fill_base_tensor(w, -1, name, kind, self.globals.ptr + 2 * off)
         self.layers: List[Pinned] = []
+        self.pinned_layers = 0
         for layer in range(w.n_layers):
-            blob = Pinned(self.layer_bytes)
+            if (layer + 1) * self.layer_bytes <= budget:
+                blob = Pinned(self.layer_bytes)
+                self.pinned_layers += 1
+            else:
+                blob = Pageable(self.layer_bytes)
             self._zero_padding(blob, cfg)
             for name in synth.LAYER_TENSORS:
                 off, _ = layer_tensor(cfg, name)

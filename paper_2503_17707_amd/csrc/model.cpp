@@ -14,10 +14,12 @@
 
 #include <algorithm>
 #include <chrono>
+#include <condition_variable>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <thread>
 #include <vector>
@@ -53,6 +55,8 @@ constexpr int MAX_RANK = 64;
 constexpr size_t VEC_ALIGN = 128;  // elements (256 bytes of dt)
 constexpr size_t GEMM_WS_BYTES = 64u << 20;  // split-K partials
 constexpr int ROW_SHRINK_MAX_TOKENS = 1024;     // fuse the q/k/v LoRA shrink up to this many tokens
+constexpr int STAGE_SLOTS = 4;                   // pinned staging ring for pageable host blobs
+constexpr size_t STAGE_BYTES = 64u << 20;        // ... bytes per slot
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -226,6 +230,20 @@ struct pb_model {
     hipEvent_t ev_globals = nullptr, ev_lora = nullptr, ev_load0 = nullptr, ev_load1 = nullptr;
     bool streamed = false, lora_recorded = false;
     double last_load_bytes = 0;
+    // loader thread (only for loads with pageable blobs): it records each
+    // layer's event as that layer's copies are enqueued; `ready` tells the
+    // forward pass, on the host, which events exist yet
+    std::thread loader;
+    std::mutex mu;
+    std::condition_variable cv;
+    std::vector<char> ready;
+    bool globals_ready = false, load_done = true;
+    int load_rc = 0;
+    std::string load_err;
+    char* ring[STAGE_SLOTS] = {};
+    hipEvent_t ring_ev[STAGE_SLOTS] = {};
+    bool ring_busy[STAGE_SLOTS] = {};
+    int ring_next = 0;
     size_t chunk_bytes = 256u << 20;
     int delay_us = 0;
     // adapter slots
@@ -387,6 +405,7 @@ int pb_model_create(const pb_config* cfg, void* dev_arena, size_t arena_bytes, v
 
 int pb_destroy(pb_model* m) {
     if (!m) return PB_OK;
+    if (m->loader.joinable()) m->loader.join();
     if (m->copy) (void)hipStreamSynchronize(m->copy);
     if (m->compute) (void)hipStreamSynchronize(m->compute);
     for (auto e : m->ev_layer)
@@ -398,6 +417,10 @@ int pb_destroy(pb_model* m) {
     for (void* p : {(void*)m->h_tokens, (void*)m->h_rowslot, (void*)m->h_scale, (void*)m->h_outtok,
                     (void*)m->h_logits})
         if (p) (void)hipHostFree(p);
+    for (int k = 0; k < STAGE_SLOTS; ++k) {
+        if (m->ring[k]) (void)hipHostFree(m->ring[k]);
+        if (m->ring_ev[k]) (void)hipEventDestroy(m->ring_ev[k]);
+    }
     delete m;
     return PB_OK;
 }
@@ -423,9 +446,94 @@ static int copy_chunked(pb_model* m, char* dst, const char* src, size_t bytes) {
     return PB_OK;
 }
 
+// Host copy split over several threads (pageable source -> pinned ring slot).
+static void parallel_memcpy(char* dst, const char* src, size_t n) {
+    const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
+    const size_t parts = std::min<size_t>(std::min(8u, hw), std::max<size_t>(1, n >> 22));
+    const size_t step = ((n + parts - 1) / parts + 4095) & ~(size_t)4095;
+    std::vector<std::thread> pool;
+    for (size_t i = 1; i < parts && i * step < n; ++i)
+        pool.emplace_back([=] { std::memcpy(dst + i * step, src + i * step, std::min(step, n - i * step)); });
+    std::memcpy(dst, src, std::min(step, n));
+    for (auto& t : pool) t.join();
+}
+
+// A pageable blob: through the pinned ring, each slot reused once its DMA
+// (an event on the copy stream) has finished.
+static int copy_staged(pb_model* m, char* dst, const char* src, size_t bytes) {
+    for (size_t o = 0; o < bytes; o += STAGE_BYTES) {
+        const size_t n = std::min(STAGE_BYTES, bytes - o);
+        const int k = m->ring_next;
+        m->ring_next = (k + 1) % STAGE_SLOTS;
+        if (m->ring_busy[k]) HIP_TRY(hipEventSynchronize(m->ring_ev[k]));
+        parallel_memcpy(m->ring[k], src + o, n);
+        HIP_TRY(hipMemcpyAsync(dst + o, m->ring[k], n, hipMemcpyHostToDevice, m->copy));
+        HIP_TRY(hipEventRecord(m->ring_ev[k], m->copy));
+        m->ring_busy[k] = true;
+    }
+    return PB_OK;
+}
+
+struct LoadJob {
+    const char* src;
+    char* dst;
+    size_t bytes;
+    bool pinned;
+    int layer;  // -1 = globals
+};
+
+// Enqueue every blob in order, recording the per-layer events; marks each
+// event as recorded for the forward pass.  Returns the first failure.
+static int run_load(pb_model* m, const std::vector<LoadJob>& jobs) {
+    for (size_t i = 0; i < jobs.size(); ++i) {
+        const LoadJob& j = jobs[i];
+        if (m->delay_us > 0 && i > 1) std::this_thread::sleep_for(std::chrono::microseconds(m->delay_us));
+        const int rc = j.pinned ? copy_chunked(m, j.dst, j.src, j.bytes) : copy_staged(m, j.dst, j.src, j.bytes);
+        if (rc) return rc;
+        HIP_TRY(hipEventRecord(j.layer < 0 ? m->ev_globals : m->ev_layer[j.layer], m->copy));
+        {
+            std::lock_guard<std::mutex> lk(m->mu);
+            if (j.layer < 0) m->globals_ready = true;
+            else m->ready[j.layer] = 1;
+        }
+        m->cv.notify_all();
+    }
+    HIP_TRY(hipEventRecord(m->ev_load1, m->copy));
+    return PB_OK;
+}
+
+static void finish_load(pb_model* m, int rc) {
+    {
+        std::lock_guard<std::mutex> lk(m->mu);
+        m->load_rc = rc;
+        m->load_err = rc ? g_err : std::string();
+        m->load_done = true;
+    }
+    m->cv.notify_all();
+}
+
+// Wait (on the host) until the event of `layer` (-1: globals) has been
+// recorded by the current load.
+static int wait_recorded(pb_model* m, int layer) {
+    std::unique_lock<std::mutex> lk(m->mu);
+    auto have = [&] { return layer < 0 ? m->globals_ready : m->ready[layer] != 0; };
+    m->cv.wait(lk, [&] { return have() || m->load_done; });
+    if (have()) return PB_OK;
+    return fail(m->load_rc ? m->load_rc : PB_ESTATE, "layer %d was not loaded: %s", layer, m->load_err.c_str());
+}
+
+// Join a previous load's thread; its failure, if any, is reported here.
+static int join_load(pb_model* m) {
+    if (m->loader.joinable()) m->loader.join();
+    if (m->load_rc) return fail(m->load_rc, "%s", m->load_err.c_str());
+    return PB_OK;
+}
+
 int pb_stream_layers(pb_model* m, const int32_t* layer_order, int32_t n_layers,
                      const void* const* host_layers, const void* host_globals) {
     if (!m) return fail(PB_EINVAL, "model is NULL");
+    if (m->loader.joinable()) m->loader.join();
+    m->load_rc = 0;
     const int L = m->cfg.n_layers;
     if (n_layers != L) return fail(PB_EINVAL, "layer_order has %d entries, the model %d layers", n_layers, L);
     if (!layer_order || !host_layers || !host_globals) return fail(PB_EINVAL, "NULL argument");
@@ -435,30 +543,56 @@ int pb_stream_layers(pb_model* m, const int32_t* layer_order, int32_t n_layers,
         if (l < 0 || l >= L || seen[l]) return fail(PB_EINVAL, "layer_order is not a permutation of 0..%d", L - 1);
         seen[l] = 1;
     }
-    const size_t lb = m->lay.layer_bytes, gb = m->gl.total * 2;
-    if (!is_pinned(host_globals, gb)) return fail(PB_ENOTPINNED, "globals blob is not pinned host memory");
     for (int l = 0; l < L; ++l)
-        if (!is_pinned(host_layers[l], lb)) return fail(PB_ENOTPINNED, "layer %d blob is not pinned host memory", l);
-    HIP_TRY(hipEventRecord(m->ev_load0, m->copy));
-    int rc = copy_chunked(m, m->at(m->lay.globals), (const char*)host_globals, gb);
-    if (rc) return rc;
-    HIP_TRY(hipEventRecord(m->ev_globals, m->copy));
+        if (!host_layers[l]) return fail(PB_EINVAL, "layer %d blob is NULL", l);
+    const size_t lb = m->lay.layer_bytes, gb = m->gl.total * 2;
+    std::vector<LoadJob> jobs;
+    jobs.push_back({(const char*)host_globals, m->at(m->lay.globals), gb, is_pinned(host_globals, gb), -1});
     for (int i = 0; i < L; ++i) {
         const int l = layer_order[i];
-        if (m->delay_us > 0 && i > 0) std::this_thread::sleep_for(std::chrono::microseconds(m->delay_us));
-        rc = copy_chunked(m, m->layer_ptr(l), (const char*)host_layers[l], lb);
-        if (rc) return rc;
-        HIP_TRY(hipEventRecord(m->ev_layer[l], m->copy));
+        jobs.push_back({(const char*)host_layers[l], m->layer_ptr(l), lb, is_pinned(host_layers[l], lb), l});
     }
-    HIP_TRY(hipEventRecord(m->ev_load1, m->copy));
+    const bool all_pinned = std::all_of(jobs.begin(), jobs.end(), [](const LoadJob& j) { return j.pinned; });
+    if (!all_pinned && !m->ring[0]) {
+        for (int k = 0; k < STAGE_SLOTS; ++k) {
+            if (hipHostMalloc((void**)&m->ring[k], STAGE_BYTES, 0) != hipSuccess)
+                return fail(PB_ENOMEM, "pinned staging ring allocation failed");
+            HIP_TRY(hipEventCreateWithFlags(&m->ring_ev[k], hipEventDisableTiming));
+        }
+    }
+    {
+        std::lock_guard<std::mutex> lk(m->mu);
+        m->ready.assign(L, 0);
+        m->globals_ready = false;
+        m->load_done = false;
+        m->load_err.clear();
+    }
+    HIP_TRY(hipEventRecord(m->ev_load0, m->copy));
     m->last_load_bytes = (double)gb + (double)L * (double)lb;
+    if (all_pinned) {
+        // every copy is a DMA from locked pages: enqueue them all now
+        const int rc = run_load(m, jobs);
+        finish_load(m, rc);
+        if (rc) return rc;
+        m->streamed = true;
+        return PB_OK;
+    }
+    // pageable blobs need host copies into the ring: a loader thread enqueues
+    // the copies in order while this call returns (the forward pass waits on
+    // the host for each layer's event to exist)
     m->streamed = true;
+    m->loader = std::thread([m, jobs = std::move(jobs)] {
+        int rc = hipSetDevice(m->device) == hipSuccess ? PB_OK : fail(PB_EHIP, "hipSetDevice failed");
+        if (!rc) rc = run_load(m, jobs);
+        finish_load(m, rc);
+    });
     return PB_OK;
 }
 
 int pb_attach_lora(pb_model* m, int32_t slot, int32_t rank, float alpha, uint32_t target_mask,
                    const void* const* host_lora) {
     if (!m) return fail(PB_EINVAL, "model is NULL");
+    if (m->loader.joinable()) m->loader.join();  // the copy stream's order stays the caller's
     const pb_config& c = m->cfg;
     if (slot < 0 || slot >= c.max_adapters) return fail(PB_EINVAL, "slot %d outside [0, %d)", slot, c.max_adapters);
     if (rank < 1 || rank > c.max_rank) return fail(PB_EINVAL, "rank %d outside [1, %d]", rank, c.max_rank);
@@ -486,6 +620,7 @@ int pb_attach_lora(pb_model* m, int32_t slot, int32_t rank, float alpha, uint32_
 
 int pb_poison_weights(pb_model* m, int32_t value) {
     if (!m) return fail(PB_EINVAL, "model is NULL");
+    if (m->loader.joinable()) m->loader.join();
     const ArenaLayout& a = m->lay;
     HIP_TRY(hipMemsetAsync(m->at(a.globals), value & 0xFF, a.loraA - a.globals, m->copy));
     // LoRA slots go back to zeros (a NaN in an unused slot would reach every
@@ -501,6 +636,7 @@ int pb_poison_weights(pb_model* m, int32_t value) {
 int pb_last_load_stats(pb_model* m, double* bytes, double* ms) {
     if (!m) return fail(PB_EINVAL, "model is NULL");
     if (!m->streamed) return fail(PB_ESTATE, "no completed pb_stream_layers");
+    if (int rc = join_load(m)) return rc;
     float t = 0.f;
     HIP_TRY(hipEventSynchronize(m->ev_load1));
     HIP_TRY(hipEventElapsedTime(&t, m->ev_load0, m->ev_load1));
@@ -578,6 +714,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
     const float* sscale = (const float*)m->at(a.slotscale);
     const pb::GemmWorkspace gws{m->at(a.ws), GEMM_WS_BYTES};
 
+    if (int rc = wait_recorded(m, -1)) return rc;
     HIP_TRY(hipStreamWaitEvent(s, m->ev_globals, 0));
     if (use_lora) HIP_TRY(hipStreamWaitEvent(s, m->ev_lora, 0));
     {
@@ -601,6 +738,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
     };
     bool ln1_ready = false;  // LN1 (and its fused shrink) of layer l produced by layer l-1's fc2 reduce
     for (int l = 0; l < L; ++l) {
+        if (int rc = wait_recorded(m, l)) return rc;
         HIP_TRY(hipStreamWaitEvent(s, m->ev_layer[l], 0));
         char* Aq = m->at(a.loraA) + (size_t)l * a.loraA_layer;  // [4][kw][d]
         char* Bq = m->at(a.loraB) + (size_t)l * a.loraB_layer;  // [4][d][kw]
@@ -682,6 +820,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             // the next layer's LN1 rides on the split-K reduce when the launcher
             // splits; its weights are read here, so wait for that layer first
             if (l + 1 < L) {
+                if (int rc = wait_recorded(m, l + 1)) return rc;
                 HIP_TRY(hipStreamWaitEvent(s, m->ev_layer[l + 1], 0));
                 p.ln_g = m->ltensor(l + 1, PB_T_LN1_G); p.ln_b = m->ltensor(l + 1, PB_T_LN1_B);
                 p.ln_out = u; p.ln_eps = c.ln_eps; p.ln_done = &ln1_ready;

@@ -34,11 +34,10 @@ def test_error_codes():
             rc = L.pb_stream_layers(m.h, arr, len(bad), ptrs, ctypes.c_void_p(hw.globals.ptr))
             assert rc == pb.PB_EINVAL, bad
             assert L.pb_last_error()
-        # pageable host memory is refused
-        pageable = np.zeros(hw.layer_bytes, np.uint8)
+        # a NULL layer blob
         arr = (ctypes.c_int32 * 2)(0, 1)
-        ptrs = (ctypes.c_void_p * 2)(pageable.ctypes.data, hw.layers[1].ptr)
-        assert L.pb_stream_layers(m.h, arr, 2, ptrs, ctypes.c_void_p(hw.globals.ptr)) == pb.PB_ENOTPINNED
+        ptrs = (ctypes.c_void_p * 2)(None, hw.layers[1].ptr)
+        assert L.pb_stream_layers(m.h, arr, 2, ptrs, ctypes.c_void_p(hw.globals.ptr)) == pb.PB_EINVAL
         # a valid stream, then argument errors of the prefill
         m.stream_layers(hw)
         with pytest.raises(pb.PbError) as e:
@@ -64,6 +63,11 @@ def test_error_codes():
         with pytest.raises(pb.PbError) as e:
             m.attach_lora(0, blobs, 5, 8.0, 5)  # rank > max_rank
         assert e.value.code == pb.PB_EINVAL
+        # LoRA blobs must be pinned
+        pageable = [pb.Pageable(b.nbytes) for b in blobs]
+        with pytest.raises(pb.PbError) as e:
+            m.attach_lora(0, pageable, 4, 8.0, 5)
+        assert e.value.code == pb.PB_ENOTPINNED
         # the model still works after every refusal
         m.attach_lora(0, blobs, 4, 8.0, 5)
         tok, logits = m.prefill(toks, [0, -1])

@@ -121,6 +121,48 @@ def test_poisoned_weights_and_late_copies_never_leak():
         hw.free()
 
 
+def test_pageable_layer_blobs_are_staged_bitwise():
+    """Layer blobs in pageable host memory go through the loader's pinned
+    staging ring on its own thread: all-pageable and half-pinned loads, with
+    poisoned device weights and late enqueues, give bit-identical results to
+    an all-pinned load."""
+    from paper_2503_17707_amd import binding as pb
+
+    w = SMALL["rot"]
+    log("case pageable layer blobs")
+    cfg = pb.make_config(w)
+    hw, m = pb.setup(w)
+    hws = [pb.HostWeights(w, cfg, pin_budget=0),
+           pb.HostWeights(w, cfg, pin_budget=(w.n_layers // 2) * hw.layer_bytes)]
+    try:
+        for h in [hw] + hws:
+            for a in sorted({a for a in w.adapters() if a >= 0}):
+                h.add_lora(a)
+        assert hws[0].pinned_layers == 0 and 0 < hws[1].pinned_layers < w.n_layers
+        toks = synth.tokens(w)
+        pb.attach_all(m, hw)
+        m.stream_layers(hw, w.order())
+        ref_tok, ref = m.prefill(toks, w.adapters())
+        for h in hws:
+            for delay in (0, 20000):
+                m.poison(0xFF)
+                m.set_stream_delay_us(delay)
+                pb.attach_all(m, h)
+                m.stream_layers(h, w.order())
+                tok, logits = m.prefill(toks, w.adapters())
+                nbytes, ms = m.load_stats()
+                log("  pinned layers %d/%d, delay %d us: load %.2f ms" % (
+                    h.pinned_layers, w.n_layers, delay, ms))
+                assert nbytes > 0 and ms > 0
+                assert np.array_equal(tok, ref_tok)
+                assert np.array_equal(logits.view(np.uint32), ref.view(np.uint32))
+        m.set_stream_delay_us(0)
+    finally:
+        m.destroy()
+        for h in [hw] + hws:
+            h.free()
+
+
 def test_mixed_batch_equals_each_sequence_alone():
     """Per-sequence adapter gather: a mixed batch gives each sequence the
     result it gets alone (up to the batch's own reduction orders: exact here,
