@@ -54,9 +54,6 @@ namespace {
 #ifndef PB_GEMM_S64
 #define PB_GEMM_S64 4  // ... of the 64 x 64 tiles
 #endif
-#ifndef PB_GEMM_T64
-#define PB_GEMM_T64 0  // 64 x 64 tiles over full K where 128 x 128 ones would need a K split
-#endif
 #ifndef PB_GEMM_S256
 #define PB_GEMM_S256 2  // ... of the 256 x 256 tiles
 #endif
@@ -374,25 +371,13 @@ hipError_t launch_resid_ln(const GemmParams& p, const SplitArgs& sa, hipStream_t
     return hipGetLastError();
 }
 
-// K split of a launch: split when the tiles alone leave CUs idle, aiming at
-// PB_GEMM_SPLIT_TARGET blocks and keeping >= PB_GEMM_MIN_KT K tiles per split
-// (256 x 256 tiles split below 256 tiles; 128 x 128 ones only below 128,
-// where the partial traffic costs less than the idle CUs).
-template <int BM, int BN>
-SplitArgs plan_split(const GemmParams& p, const GemmWorkspace& wsp, int tiles) {
+// K split into `splits` ranges: splits 0..S-2 take kt_split base tiles each,
+// the last one the rest (and the LoRA tiles); S = ceil(nk1 / kt_split) leaves
+// no split empty.
+SplitArgs make_split(const GemmParams& p, const GemmWorkspace& wsp, int splits) {
     const int nk1 = p.K1 / BK;
-    int splits = 1;
-    constexpr int split_below = (BM == 128 && BN == 128) ? 128 : 256;
-    if (tiles < split_below && wsp.ws && wsp.bytes > 0) {
-        splits = std::min((PB_GEMM_SPLIT_TARGET + tiles - 1) / tiles, nk1 / PB_GEMM_MIN_KT);
-        const int64_t per_split = (int64_t)p.M * p.N * 4;
-        splits = (int)std::min<int64_t>(splits, (int64_t)(wsp.bytes / per_split));
-        if (splits < 1) splits = 1;
-    }
     SplitArgs sa;
     sa.kt_split = (nk1 + splits - 1) / splits;
-    // splits 0..S-2 take kt_split base tiles each, the last one the rest (and
-    // the LoRA tiles); S = ceil(nk1 / kt_split) leaves no split empty
     sa.splits = (nk1 + sa.kt_split - 1) / sa.kt_split;
     sa.ws = (float*)wsp.ws;
     return sa;
@@ -414,7 +399,7 @@ hipError_t finish_split(const GemmParams& p, const SplitArgs& sa, hipStream_t s)
 }
 
 template <typename T, int EPI, int BM, int BN, int WGM, int WGN, int ROLE, int S>
-hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t s) {
+hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, int splits, hipStream_t s) {
     constexpr int LDS = S * (BM + BN) * ROW_BYTES;
     static bool attr_set = false;
     if (!attr_set) {
@@ -424,7 +409,7 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t
         attr_set = true;
     }
     const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
-    const SplitArgs sa = plan_split<BM, BN>(p, wsp, tiles);
+    const SplitArgs sa = make_split(p, wsp, splits);
     hipLaunchKernelGGL((gemm_kernel<T, EPI, BM, BN, WGM, WGN, ROLE, S>), dim3(tiles * sa.splits),
                        dim3(64 * WGM * WGN), LDS, s, p, sa);
     const hipError_t e = hipGetLastError();
@@ -432,16 +417,55 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t
     return finish_split<T, EPI, ROLE>(p, sa, s);
 }
 
+// Tile shape and K split of a launch, from a cost model: a block's time is
+// its MFMA work at the rate one CU reaches with that tile (measured: 256 x 256
+// ~4.5 TFLOP/s, 128 x 128 ~2.6), blocks run in rounds of 256 (one per CU), and
+// a split adds its fp32 partials (written, then read by the reduce) at
+// ~4 TB/s.  Splits keep >= PB_GEMM_MIN_KT K tiles each and fit the workspace.
+struct TilePlan {
+    int tile;    // 256, 128 or 64
+    int splits;
+};
+
+TilePlan plan_tiles(const GemmParams& p, const GemmWorkspace& wsp) {
+    const int nk1 = p.K1 / BK;
+    const double out_bytes = (double)p.M * p.N * 4;
+    TilePlan best{64, 1};
+    double best_t = 1e30;
+    auto consider = [&](int t, double rate) {
+        if (p.N % t) return;
+        const long tiles = (long)((p.M + t - 1) / t) * (p.N / t);
+        for (int s = 1; s <= 8; ++s) {
+            if (s > 1 && (nk1 / s < PB_GEMM_MIN_KT || !wsp.ws || out_bytes * s > (double)wsp.bytes)) break;
+            const long rounds = (tiles * s + 255) / 256;
+            const double k = (double)p.K1 / s;
+            const double tt = rounds * (2.0 * t * t * k / rate) + (s > 1 ? 2.0 * out_bytes * s / 4e12 : 0.0);
+            if (tt < best_t * 0.98) {  // prefer the simpler plan on near ties
+                best_t = tt;
+                best = {t, s};
+            }
+        }
+    };
+    consider(256, 4.5e12);
+    consider(128, 2.6e12);
+    if (best_t >= 1e30) {  // N not a multiple of 128: 64 x 64 tiles, split when few
+        const long tiles = (long)((p.M + 63) / 64) * (p.N / 64);
+        int s = 1;
+        if (tiles < 256 && wsp.ws) {
+            s = std::min<long>((PB_GEMM_SPLIT_TARGET + tiles - 1) / tiles, std::max(1, nk1 / PB_GEMM_MIN_KT));
+            while (s > 1 && out_bytes * s > (double)wsp.bytes) --s;
+        }
+        best = {64, std::max(1, s)};
+    }
+    return best;
+}
+
 template <typename T, int EPI, int ROLE>
 hipError_t launch_tiles(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t s) {
-    auto tiles = [&](int bm, int bn) { return (long)((p.M + bm - 1) / bm) * ((p.N + bn - 1) / bn); };
-    // 256 x 256 when those tiles fill the GPU, or half fill it over a long K
-    // (then split along K); else 128 x 128 (split along K when too few)
-    if (p.N % 256 == 0 && (tiles(256, 256) >= 256 || (tiles(256, 256) >= 128 && p.K1 >= 8192)))
-        return launch_cfg<T, EPI, 256, 256, 2, 4, ROLE, PB_GEMM_S256>(p, wsp, s);
-    const bool small64 = PB_GEMM_T64 && tiles(128, 128) < 128 && tiles(64, 64) >= 256;
-    if (p.N % 128 == 0 && !small64) return launch_cfg<T, EPI, 128, 128, 2, 4, ROLE, PB_GEMM_S128>(p, wsp, s);
-    return launch_cfg<T, EPI, 64, 64, 2, 2, ROLE, PB_GEMM_S64>(p, wsp, s);
+    const TilePlan tp = plan_tiles(p, wsp);
+    if (tp.tile == 256) return launch_cfg<T, EPI, 256, 256, 2, 4, ROLE, PB_GEMM_S256>(p, wsp, tp.splits, s);
+    if (tp.tile == 128) return launch_cfg<T, EPI, 128, 128, 2, 4, ROLE, PB_GEMM_S128>(p, wsp, tp.splits, s);
+    return launch_cfg<T, EPI, 64, 64, 2, 2, ROLE, PB_GEMM_S64>(p, wsp, tp.splits, s);
 }
 
 template <typename T>
@@ -451,7 +475,15 @@ hipError_t launch_typed(int role, const GemmParams& p, const GemmWorkspace& wsp,
         case 1: return launch_tiles<T, EPI_RESID, 1>(p, wsp, s);
         case 2: return launch_tiles<T, EPI_RELU, 2>(p, wsp, s);
         case 3: return launch_tiles<T, EPI_RESID, 3>(p, wsp, s);
-        case 4: return launch_cfg<T, EPI_SHRINK, 64, 64, 2, 2, 4, 4>(p, wsp, s);
+        case 4: {  // LoRA shrink: 64 x 64 tiles, split along K when few
+            const long tiles = (long)((p.M + 63) / 64) * (p.N / 64);
+            int sp = 1;
+            if (tiles < 256 && wsp.ws) {
+                sp = std::min<long>((PB_GEMM_SPLIT_TARGET + tiles - 1) / tiles, std::max(1, p.K1 / BK / PB_GEMM_MIN_KT));
+                while (sp > 1 && (double)p.M * p.N * 4 * sp > (double)wsp.bytes) --sp;
+            }
+            return launch_cfg<T, EPI_SHRINK, 64, 64, 2, 2, 4, 4>(p, wsp, std::max(1, sp), s);
+        }
         default: break;
     }
     return hipErrorInvalidValue;

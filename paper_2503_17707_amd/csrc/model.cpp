@@ -53,7 +53,12 @@ constexpr size_t ALIGN = 256;
 constexpr int MAX_SLOTS = 16;
 constexpr int MAX_RANK = 64;
 constexpr size_t VEC_ALIGN = 128;  // elements (256 bytes of dt)
-constexpr size_t GEMM_WS_BYTES = 64u << 20;  // split-K partials
+// split-K partials: room for 4 fp32 partials of a [max_tokens, d_model]
+// output (the o and fc2 projections), between 64 MiB and 1 GiB
+size_t gemm_ws_bytes(const pb_config* c) {
+    const size_t want = (size_t)4 * c->max_tokens * c->d_model * 4;
+    return std::min<size_t>(std::max<size_t>(want, 64u << 20), 1u << 30);
+}
 constexpr int ROW_SHRINK_MAX_TOKENS = 1024;     // fuse the q/k/v LoRA shrink up to this many tokens
 constexpr int STAGE_SLOTS = 4;                   // pinned staging ring for pageable host blobs
 constexpr size_t STAGE_BYTES = 64u << 20;        // ... bytes per slot
@@ -156,7 +161,7 @@ struct ArenaLayout {
     size_t globals, layers, layer_bytes, loraA, loraB, loraA_layer, loraB_layer;
     size_t x, u, qkv, attn, h, z, rowslot, tokens, slotscale, zf, logits, outtok, staging, ws;
     size_t pval, pidx;
-    size_t staging_bytes, total;
+    size_t staging_bytes, ws_bytes, total;
 };
 
 ArenaLayout arena_layout(const pb_config* c) {
@@ -195,7 +200,8 @@ ArenaLayout arena_layout(const pb_config* c) {
     a.pidx = take(B * (size_t)pb::lm_head_blocks((int)V) * 4);
     a.staging_bytes = c->max_adapters > 0 ? L * lora_layer_elems(c, c->max_rank, 0xF) * 2 : 0;
     a.staging = take(a.staging_bytes);
-    a.ws = take(GEMM_WS_BYTES);
+    a.ws_bytes = gemm_ws_bytes(c);
+    a.ws = take(a.ws_bytes);
     a.total = align_up(p, ALIGN);
     return a;
 }
@@ -712,7 +718,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
     const int kw = a.kw;
     const int32_t* rowslot = (const int32_t*)m->at(a.rowslot);
     const float* sscale = (const float*)m->at(a.slotscale);
-    const pb::GemmWorkspace gws{m->at(a.ws), GEMM_WS_BYTES};
+    const pb::GemmWorkspace gws{m->at(a.ws), a.ws_bytes};
 
     if (int rc = wait_recorded(m, -1)) return rc;
     HIP_TRY(hipStreamWaitEvent(s, m->ev_globals, 0));
