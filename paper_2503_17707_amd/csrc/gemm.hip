@@ -176,8 +176,11 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, const SplitArgs&
     }
 }
 
+// (at least two waves per SIMD as the register budget: with more registers the
+// compiler moves accumulators between register files around every MFMA)
 template <typename T, int EPI, int BM, int BN, int WGM, int WGN, int ROLE, int S>
-__global__ __launch_bounds__(64 * WGM * WGN) void gemm_kernel(GemmParams p, SplitArgs sa) {
+__global__ __launch_bounds__(64 * WGM * WGN) __attribute__((amdgpu_waves_per_eu(2)))
+void gemm_kernel(GemmParams p, SplitArgs sa) {
     typedef typename Mfma<T>::vec8 vec8;
     constexpr int NW = WGM * WGN;               // waves per block
     constexpr int WM = BM / WGM, WN = BN / WGN;  // wave tile
