@@ -124,8 +124,21 @@ def oracle_baseline(w, n_layers):
     flops = per_layer * n_layers + fl["lm_head"]
     cores = len(os.sched_getaffinity(0))
     threads = int(os.environ.get("OMP_NUM_THREADS", cores))
+    cpu_model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        b = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        blas = ("%s %s" % (b.get("name", ""), b.get("version", ""))).strip()
+    except Exception:
+        blas = "unknown"
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": min(cores, threads),
-            "kind": "oracle", "seconds": dt,
+            "kind": "oracle", "seconds": dt, "cpu_model": cpu_model, "blas": blas,
             "sample": "float64 numpy oracle, first %d of %d layers of the same workload "
                       "(B=%d, T=%d) plus final LayerNorm and LM head; weight draws made before "
                       "timing, widening to float64 timed" % (n_layers, w.n_layers, w.batch,
@@ -230,8 +243,9 @@ def main():
     hw = pb.HostWeights(w, cfg)
     for a in sorted({a for a in w.adapters() if a >= 0}):
         hw.add_lora(a)
-    err("host weights: %.1f GB pinned in %.1f s" % (
-        (hw.globals_bytes + len(hw.layers) * hw.layer_bytes) / 1e9, time.perf_counter() - t0))
+    err("host weights: %.1f GB (%d of %d layer blobs pinned, the rest staged) in %.1f s" % (
+        (hw.globals_bytes + len(hw.layers) * hw.layer_bytes) / 1e9, hw.pinned_layers,
+        len(hw.layers), time.perf_counter() - t0))
     t0 = time.perf_counter()
     m = pb.Model(cfg, "cuda:0")
     init_ms = (time.perf_counter() - t0) * 1e3

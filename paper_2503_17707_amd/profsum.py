@@ -108,18 +108,23 @@ def overlap(d, label):
 
 def mfma(d, label):
     per = collections.defaultdict(lambda: collections.defaultdict(list))
+    dur = collections.defaultdict(dict)  # kind -> dispatch -> ns
     for r in csv.DictReader(open(_one(d, "*counter_collection.csv"))):
         k = kind_of(r["Kernel_Name"])
         if k:
             per[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+            dur[k][r["Dispatch_Id"]] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
     out = ["# MFMA work and matrix-unit busy fraction per kernel kind, %s\n" % label,
            "Counters per dispatch, averaged over the run's dispatches of each kind.  MFMA "
            "FLOPs = SQ_INSTS_VALU_MFMA_MOPS_F16 x 512.  Busy = SQ_VALU_MFMA_BUSY_CYCLES / "
            "(GRBM_GUI_ACTIVE / %d XCDs x %d SIMDs): the share of all SIMD cycles, over the "
            "dispatch, in which the matrix unit was busy.  Counter runs serialize dispatches, so "
-           "launch gaps are absent here.\n" % (N_XCD, N_SIMD),
+           "launch gaps are absent here.  Clock = GRBM_GUI_ACTIVE / %d XCDs / the dispatch's "
+           "duration: the sustained shader clock, read from the long dispatches (GRBM_GUI_ACTIVE also counts "
+           "the counters' own start and stop, which dominates dispatches of a few microseconds and "
+           "inflates their clock and deflates their busy share).\n" % (N_XCD, N_SIMD, N_XCD),
            "| kind | dispatches | MFMA GFLOP per dispatch | GPU cycles per dispatch | "
-           "MFMA busy |", "|---|---|---|---|---|"]
+           "clock GHz | MFMA busy |", "|---|---|---|---|---|---|"]
     for k in sorted(per):
         c = per[k]
         if not c.get("GRBM_GUI_ACTIVE"):
@@ -128,8 +133,9 @@ def mfma(d, label):
         mops = sum(c.get("SQ_INSTS_VALU_MFMA_MOPS_F16", [0])) / n
         busy = sum(c.get("SQ_VALU_MFMA_BUSY_CYCLES", [0])) / n
         gui = sum(c["GRBM_GUI_ACTIVE"]) / n / N_XCD
-        out.append("| %s | %d | %.3f | %.0f | %.3f |" % (k, n, mops * 512 / 1e9, gui,
-                                                          busy / (gui * N_SIMD) if gui else 0.0))
+        ns = sum(dur[k].values()) / max(1, len(dur[k]))
+        out.append("| %s | %d | %.3f | %.0f | %.2f | %.3f |" % (
+            k, n, mops * 512 / 1e9, gui, gui / ns if ns else 0.0, busy / (gui * N_SIMD) if gui else 0.0))
     return "\n".join(out)
 
 

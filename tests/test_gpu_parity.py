@@ -46,6 +46,21 @@ def test_small_workload_matches_oracle(name):
     compare(name, logits, tok, ref_logits, ref_tok)
 
 
+def test_tiny_storage_rounding_and_kernel_error_apart():
+    """The tiny decoder's oracle runs on the float32 draws while the GPU stores
+    their bf16 rounding; the oracle on the bf16-widened weights isolates the
+    kernels' own error from that storage rounding.  Both are logged, both are
+    within tolerance."""
+    w = SMALL["tiny"]
+    log("case tiny: storage rounding vs kernel error")
+    tok, logits = run_gpu(w)
+    ref32, tok32 = oracle.prefill_first_token(w)
+    ref16, tok16 = oracle.prefill_first_token(w.with_(oracle_weights="storage"))
+    d32 = compare("tiny vs oracle on f32 draws", logits, tok, ref32, tok32)
+    d16 = compare("tiny vs oracle on bf16 weights", logits, tok, ref16, tok16)
+    log("  storage + kernel max|d| %.2e, kernel alone %.2e" % (d32[0], d16[0]))
+
+
 def test_lora_with_zero_b_is_bit_identical_to_base():
     w = SMALL["mixed"].with_(lora_zero_b=True)
     log("case lora_zero_b")
