@@ -1,11 +1,13 @@
 """Summaries of rocprofv3 CSV output for the cold-start path (markdown on stdout).
 
-  python -m paper_2503_17707_amd.profsum overlap DIR LABEL
+  python -m paper_2503_17707_amd.profsum overlap DIR LABEL [GAP_MS]
       DIR from `rocprofv3 --kernel-trace --memory-copy-trace -f csv -d DIR -o ov
       -- python bench.py ...`: for every cold start in the run (a burst of
       host-to-device copies followed by the library's kernels), how much of the
       compute ran while weights were still being copied, and the compute tail
-      left after the last copy.
+      left after the last copy.  Copies further apart than GAP_MS (default
+      0.35) start a new load: raise it when staged copies of pageable blobs
+      leave longer gaps inside one load.
 
   python -m paper_2503_17707_amd.profsum mfma DIR LABEL
       DIR from `rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_F16 SQ_VALU_MFMA_BUSY_CYCLES
@@ -24,7 +26,7 @@ import sys
 
 N_XCD = 8           # GRBM_GUI_ACTIVE is summed over the 8 XCDs
 N_SIMD = 256 * 4    # SQ_VALU_MFMA_BUSY_CYCLES is summed over every SIMD
-GAP_NS = 350_000  # copies further apart than this start a new load (within a load: < 0.25 ms)
+GAP_NS = 350_000  # default: copies further apart start a new load (pinned loads: gaps < 0.25 ms)
 
 
 def _one(d, pattern):
@@ -66,7 +68,7 @@ def _inter(u, lo, hi):
     return sum(max(0, min(e, hi) - max(s, lo)) for s, e in u)
 
 
-def overlap(d, label):
+def overlap(d, label, gap_ns=GAP_NS):
     copies = [(int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
               for r in csv.DictReader(open(_one(d, "*memory_copy_trace.csv")))
               if r["Direction"].endswith("HOST_TO_DEVICE")]
@@ -75,7 +77,7 @@ def overlap(d, label):
     copies.sort()
     loads = []
     for s, e in copies:
-        if loads and s - loads[-1][1] < GAP_NS:
+        if loads and s - loads[-1][1] < gap_ns:
             loads[-1][1] = max(loads[-1][1], e)
             loads[-1][2] += 1
         else:
@@ -140,10 +142,13 @@ def mfma(d, label):
 
 
 def main(argv):
-    if len(argv) != 3 or argv[0] not in ("overlap", "mfma"):
+    if len(argv) < 3 or argv[0] not in ("overlap", "mfma") or (argv[0] == "mfma" and len(argv) != 3):
         raise SystemExit(__doc__)
-    fn = overlap if argv[0] == "overlap" else mfma
-    print(fn(argv[1], argv[2]))
+    if argv[0] == "overlap":
+        gap = int(float(argv[3]) * 1e6) if len(argv) > 3 else GAP_NS
+        print(overlap(argv[1], argv[2], gap))
+    else:
+        print(mfma(argv[1], argv[2]))
 
 
 if __name__ == "__main__":
