@@ -380,7 +380,7 @@ class Model:
 
 
 def setup(w, device: str = "cuda:0", hw: Optional[HostWeights] = None, **cap):
-    """Create host blobs (pinned), a model, and attach the workload's adapters (slots 0..)."""
+    """Create the host blobs (layer blobs pinned up to the budget) and a model."""
     cfg = make_config(w, **cap)
     hw = hw or HostWeights(w, cfg)
     m = Model(cfg, device)
