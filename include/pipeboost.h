@@ -74,6 +74,8 @@ typedef struct {
     int32_t max_rank;     /* largest LoRA rank a slot may hold */
     int32_t dtype;        /* pb_dtype */
     float ln_eps;         /* LayerNorm epsilon (1e-5 for OPT) */
+    int32_t max_new_tokens; /* decode steps after a prefill; > 0 keeps a KV cache of
+                               [n_layers][max_batch][max_pos][2 d_model] in the arena */
 } pb_config;
 
 typedef struct pb_model pb_model;
@@ -173,6 +175,19 @@ int pb_attach_lora(pb_model* m, int32_t slot, int32_t rank, float alpha, uint32_
  * the argmax go to the lowest token id. */
 int pb_prefill_first_token(pb_model* m, const int32_t* tokens, int32_t B, int32_t T,
                            const int32_t* adapter_of_seq, int32_t* out_tokens, float* out_logits);
+
+/* Decode stage (Section 2.1): one more token for each sequence of the last
+ * prefill, attending to the KV cache that prefill and earlier steps filled.
+ * tokens: host int32 [B], the newest token of each sequence (the previous
+ * call's out_tokens to continue greedily); it takes position T + steps so far
+ * and its keys and values join the cache.  adapter_of_seq must equal the
+ * prefill's.  out_tokens / out_logits as for the prefill.  Requires a model
+ * created with max_new_tokens > 0 and a prior successful prefill of the same
+ * B (PB_ESTATE / PB_EINVAL otherwise); at most max_new_tokens steps, and the
+ * sequences stay within max_pos positions (PB_ESTATE).  Blocks until the
+ * outputs are in host memory. */
+int pb_decode_step(pb_model* m, const int32_t* tokens, int32_t B, const int32_t* adapter_of_seq,
+                   int32_t* out_tokens, float* out_logits);
 
 /* Release the model's events and staging (not the caller's arena or streams). */
 int pb_destroy(pb_model* m);

@@ -40,7 +40,8 @@ class Config(ctypes.Structure):
                 ("vocab", ctypes.c_int32), ("max_pos", ctypes.c_int32),
                 ("max_tokens", ctypes.c_int32), ("max_batch", ctypes.c_int32),
                 ("max_adapters", ctypes.c_int32), ("max_rank", ctypes.c_int32),
-                ("dtype", ctypes.c_int32), ("ln_eps", ctypes.c_float)]
+                ("dtype", ctypes.c_int32), ("ln_eps", ctypes.c_float),
+                ("max_new_tokens", ctypes.c_int32)]
 
 
 _SIGS = {
@@ -70,6 +71,9 @@ _SIGS = {
     "pb_attach_lora": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                       ctypes.c_float, ctypes.c_uint32,
                                       ctypes.POINTER(ctypes.c_void_p)]),
+    "pb_decode_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
+                                      ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
+                                      ctypes.POINTER(ctypes.c_float)]),
     "pb_prefill_first_token": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32),
                                               ctypes.c_int32, ctypes.c_int32,
                                               ctypes.POINTER(ctypes.c_int32),
@@ -130,15 +134,18 @@ def check(rc: int) -> None:
 
 
 def make_config(w, max_tokens: Optional[int] = None, max_batch: Optional[int] = None,
-                max_adapters: Optional[int] = None, max_rank: Optional[int] = None) -> Config:
-    """pb_config of a synth.Workload (capacities default to the workload's own sizes)."""
+                max_adapters: Optional[int] = None, max_rank: Optional[int] = None,
+                max_new_tokens: int = 0) -> Config:
+    """pb_config of a synth.Workload (capacities default to the workload's own sizes;
+    max_new_tokens > 0 adds a KV cache for decode steps)."""
     return Config(n_layers=w.n_layers, d_model=w.d_model, n_heads=w.n_heads, d_ffn=w.d_ffn,
                   vocab=w.vocab, max_pos=w.max_pos,
                   max_tokens=max_tokens or w.batch * w.seq_len,
                   max_batch=max_batch or w.batch,
                   max_adapters=w.n_adapters if max_adapters is None else max_adapters,
                   max_rank=max_rank or w.lora_rank,
-                  dtype=PB_BF16 if w.dtype == "bf16" else PB_F16, ln_eps=w.ln_eps)
+                  dtype=PB_BF16 if w.dtype == "bf16" else PB_F16, ln_eps=w.ln_eps,
+                  max_new_tokens=max_new_tokens)
 
 
 def layer_tensor(cfg: Config, name: str):
@@ -335,6 +342,23 @@ class Model:
             ad = ad_arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
         check(lib().pb_prefill_first_token(
             self.h, tokens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), B, T, ad,
+            out_tok.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+            logits.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if want_logits else None))
+        return out_tok, logits
+
+    def decode(self, tokens: np.ndarray, adapter_of_seq: Optional[Sequence[int]] = None,
+               want_logits: bool = True):
+        """One decode step: tokens [B] (the newest token of each sequence)."""
+        tokens = np.ascontiguousarray(tokens, dtype=np.int32).reshape(-1)
+        B = tokens.shape[0]
+        out_tok = np.empty(B, dtype=np.int32)
+        logits = np.empty((B, self.cfg.vocab), dtype=np.float32) if want_logits else None
+        ad = None
+        if adapter_of_seq is not None:
+            ad_arr = np.ascontiguousarray(adapter_of_seq, dtype=np.int32)
+            ad = ad_arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        check(lib().pb_decode_step(
+            self.h, tokens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), B, ad,
             out_tok.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
             logits.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if want_logits else None))
         return out_tok, logits

@@ -284,6 +284,119 @@ hipError_t launch_qw(const void* qkv, void* out, int B, int T_len, int H, hipStr
     return launch_hd<T, HD, 16>(qkv, out, B, T_len, H, s);
 }
 
+
+// ---- decode: one new query per (sequence, head) against the KV cache --------
+// Split over keys (256 per block, 64 per wave): each lane scores one key
+// (fp32 dot product with the query, held in LDS), each wave takes its own max
+// and sum, then lanes switch to head dimensions to accumulate P V over the
+// wave's keys.  Blocks write (max, sum, o) partials; a second kernel combines
+// the splits of each (sequence, head) in split order.
+constexpr int DEC_KEYS = 256;
+
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void decode_attention_kernel(const T* __restrict__ qkv,
+                                                              const T* __restrict__ kv,
+                                                              int64_t seq_stride, int d, int nkeys,
+                                                              float* __restrict__ part, int nsplit) {
+    constexpr int DPL = HD / 64;  // head dimensions per lane in the P V product
+    __shared__ float qs[HD];
+    __shared__ float ps[4][64];
+    __shared__ float wm[4], wl[4];
+    __shared__ float wo[4][HD];
+    const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    const int H = gridDim.y;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const T* q = qkv + (int64_t)b * 3 * d + h * HD;
+    for (int i = threadIdx.x; i < HD; i += 256) qs[i] = (float)q[i];
+    __syncthreads();
+    const T* kvb = kv + (int64_t)b * seq_stride;
+    const int kbase = split * DEC_KEYS + wave * 64;
+    const int key = kbase + lane;
+    const bool valid = key < nkeys;
+    const T* krow = kvb + (int64_t)min(key, nkeys - 1) * 2 * d + h * HD;
+    float sc = 0.f;
+#pragma unroll
+    for (int c = 0; c < HD; c += 8) {
+        const u32x4 raw = *(const u32x4*)(krow + c);
+        T e[8];
+        __builtin_memcpy(e, &raw, 16);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) sc += (float)e[j] * qs[c + j];
+    }
+    sc = valid ? sc : -INFINITY;
+    const float m = wave_max(sc);  // -inf only for a wave with no key
+    const float pk = valid ? __builtin_amdgcn_exp2f((sc - m) * LOG2E) : 0.f;
+    const float l = wave_sum(pk);
+    ps[wave][lane] = pk;
+    __syncthreads();
+    float o[DPL];
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) o[e] = 0.f;
+    const int nk = max(0, min(64, nkeys - kbase));
+    for (int j = 0; j < nk; ++j) {
+        const T* vrow = kvb + (int64_t)(kbase + j) * 2 * d + d + h * HD + lane * DPL;
+        const float p = ps[wave][j];
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) o[e] += p * (float)vrow[e];
+    }
+    if (lane == 0) {
+        wm[wave] = m;
+        wl[wave] = l;
+    }
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) wo[wave][lane * DPL + e] = o[e];
+    __syncthreads();
+    if (threadIdx.x < HD) {
+        const int dim = threadIdx.x;
+        const float M = fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3]));
+        float acc = 0.f, L = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            if (wm[w] == -INFINITY) continue;
+            const float f = __builtin_amdgcn_exp2f((wm[w] - M) * LOG2E);
+            acc += f * wo[w][dim];
+            L += f * wl[w];
+        }
+        float* out = part + (((int64_t)b * H + h) * nsplit + split) * (HD + 2);
+        out[2 + dim] = acc;
+        if (dim == 0) {
+            out[0] = M;
+            out[1] = L;
+        }
+    }
+}
+
+template <typename T, int HD>
+__global__ __launch_bounds__(HD) void decode_combine_kernel(const float* __restrict__ part, int nsplit,
+                                                           int d, T* __restrict__ out) {
+    const int h = blockIdx.x, b = blockIdx.y, H = gridDim.x;
+    const int dim = threadIdx.x;
+    const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
+    float M = -INFINITY;
+    for (int sp = 0; sp < nsplit; ++sp) M = fmaxf(M, pp[sp * (HD + 2)]);
+    float acc = 0.f, L = 0.f;
+    for (int sp = 0; sp < nsplit; ++sp) {
+        const float ms = pp[sp * (HD + 2)];
+        if (ms == -INFINITY) continue;
+        const float f = __builtin_amdgcn_exp2f((ms - M) * LOG2E);
+        acc += f * pp[sp * (HD + 2) + 2 + dim];
+        L += f * pp[sp * (HD + 2) + 1];
+    }
+    out[(int64_t)b * d + h * HD + dim] = (T)(acc / L);
+}
+
+template <typename T, int HD>
+hipError_t launch_decode_hd(const void* qkv, const void* kv, int64_t seq_stride, int B, int H, int nkeys,
+                            float* part, void* out, hipStream_t s) {
+    const int d = H * HD;
+    const int nsplit = (nkeys + DEC_KEYS - 1) / DEC_KEYS;
+    hipLaunchKernelGGL((decode_attention_kernel<T, HD>), dim3(nsplit, H, B), dim3(256), 0, s, (const T*)qkv,
+                       (const T*)kv, seq_stride, d, nkeys, part, nsplit);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((decode_combine_kernel<T, HD>), dim3(H, B), dim3(HD), 0, s, part, nsplit, d, (T*)out);
+    return hipGetLastError();
+}
 }  // namespace
 
 hipError_t launch_attention(int dtype, const void* qkv, void* out, int B, int T_len, int H,
@@ -296,6 +409,25 @@ hipError_t launch_attention(int dtype, const void* qkv, void* out, int B, int T_
     } else {
         if (hd == 64) return launch_qw<__bf16, 64>(qkv, out, B, T_len, H, s);
         if (hd == 128) return launch_qw<__bf16, 128>(qkv, out, B, T_len, H, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+size_t decode_attention_part_floats(int B, int H, int hd, int max_keys) {
+    return (size_t)B * H * ((max_keys + DEC_KEYS - 1) / DEC_KEYS) * (hd + 2);
+}
+
+hipError_t launch_decode_attention(int dtype, const void* qkv, const void* kv, int64_t seq_stride,
+                                   int B, int H, int hd, int nkeys, float* part, void* out,
+                                   hipStream_t s) {
+    if (B <= 0) return hipSuccess;
+    if (nkeys <= 0) return hipErrorInvalidValue;
+    if (dtype == 1) {
+        if (hd == 64) return launch_decode_hd<_Float16, 64>(qkv, kv, seq_stride, B, H, nkeys, part, out, s);
+        if (hd == 128) return launch_decode_hd<_Float16, 128>(qkv, kv, seq_stride, B, H, nkeys, part, out, s);
+    } else {
+        if (hd == 64) return launch_decode_hd<__bf16, 64>(qkv, kv, seq_stride, B, H, nkeys, part, out, s);
+        if (hd == 128) return launch_decode_hd<__bf16, 128>(qkv, kv, seq_stride, B, H, nkeys, part, out, s);
     }
     return hipErrorInvalidValue;
 }

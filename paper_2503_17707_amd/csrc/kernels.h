@@ -62,7 +62,19 @@ hipError_t launch_attention(int dtype, const void* qkv, void* out, int B, int T,
 
 // x[b*T + t, :] = E[tok[b*T + t], :] + P[t, :] (fp32 output).
 hipError_t launch_embed(int dtype, const int32_t* tok, const void* E, const void* P, float* x,
-                        int n_rows, int T, int d, hipStream_t s);
+                        int n_rows, int T, int d, hipStream_t s, int pos0 = 0);
+
+// Keys and values of n_rows token rows of qkv into the KV cache (see misc.hip).
+hipError_t launch_kv_store(int dtype, const void* qkv, int n_rows, int T_len, int pos0, int d,
+                           void* kv, int64_t seq_stride, hipStream_t s);
+
+// One new query per (sequence, head) of qkv ([B, 3d], q pre-scaled) against
+// cache positions 0 .. nkeys-1 of kv ([B][seq_stride], rows [k | v] of 2d);
+// out [B, d].  part: scratch of decode_attention_part_floats(B, H, hd, nkeys).
+size_t decode_attention_part_floats(int B, int H, int hd, int max_keys);
+hipError_t launch_decode_attention(int dtype, const void* qkv, const void* kv, int64_t seq_stride,
+                                   int B, int H, int hd, int nkeys, float* part, void* out,
+                                   hipStream_t s);
 
 // out[r, :] = LN(x[r * in_mul + in_add, :]) * g + b, fp32 statistics;
 // out_f32 selects a float output, otherwise dt.

@@ -14,9 +14,10 @@ template <typename T>
 __global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ tok,
                                                    const T* __restrict__ E,
                                                    const T* __restrict__ P,
-                                                   float* __restrict__ x, int T_len, int d) {
+                                                   float* __restrict__ x, int T_len, int d,
+                                                   int pos0) {
     const int row = blockIdx.x;
-    const int t = row % T_len;
+    const int t = pos0 + row % T_len;
     const T* e = E + (int64_t)tok[row] * d;
     const T* pp = P + (int64_t)t * d;
     float* xr = x + (int64_t)row * d;
@@ -246,14 +247,39 @@ __global__ __launch_bounds__(256) void lora_pack_kernel(const T* __restrict__ st
 }  // namespace
 
 hipError_t launch_embed(int dtype, const int32_t* tok, const void* E, const void* P, float* x,
-                        int n_rows, int T_len, int d, hipStream_t s) {
+                        int n_rows, int T_len, int d, hipStream_t s, int pos0) {
     if (n_rows <= 0) return hipSuccess;
     if (dtype == 1)
         hipLaunchKernelGGL(embed_kernel<_Float16>, dim3(n_rows), dim3(256), 0, s, tok,
-                           (const _Float16*)E, (const _Float16*)P, x, T_len, d);
+                           (const _Float16*)E, (const _Float16*)P, x, T_len, d, pos0);
     else
         hipLaunchKernelGGL(embed_kernel<__bf16>, dim3(n_rows), dim3(256), 0, s, tok,
-                           (const __bf16*)E, (const __bf16*)P, x, T_len, d);
+                           (const __bf16*)E, (const __bf16*)P, x, T_len, d, pos0);
+    return hipGetLastError();
+}
+
+// ---- KV cache: keys and values of token rows into their cache positions ----
+// Row r of qkv ([N, 3d], sequence-major, T_len rows per sequence) holds the
+// key at columns [d, 2d) and the value at [2d, 3d); they go to cache row
+// (sequence r / T_len, position pos0 + r % T_len) of kv ([B][seq_rows][2d]).
+template <typename T>
+__global__ __launch_bounds__(256) void kv_store_kernel(const T* __restrict__ qkv, int d, int T_len,
+                                                      int pos0, T* __restrict__ kv, int64_t seq_stride) {
+    const int r = blockIdx.x;
+    const T* src = qkv + (int64_t)r * 3 * d + d;
+    T* dst = kv + (int64_t)(r / T_len) * seq_stride + (int64_t)(pos0 + r % T_len) * 2 * d;
+    for (int c = threadIdx.x * 8; c < 2 * d; c += 256 * 8) *(u32x4*)(dst + c) = *(const u32x4*)(src + c);
+}
+
+hipError_t launch_kv_store(int dtype, const void* qkv, int n_rows, int T_len, int pos0, int d,
+                           void* kv, int64_t seq_stride, hipStream_t s) {
+    if (n_rows <= 0) return hipSuccess;
+    if (dtype == 1)
+        hipLaunchKernelGGL(kv_store_kernel<_Float16>, dim3(n_rows), dim3(256), 0, s,
+                           (const _Float16*)qkv, d, T_len, pos0, (_Float16*)kv, seq_stride);
+    else
+        hipLaunchKernelGGL(kv_store_kernel<__bf16>, dim3(n_rows), dim3(256), 0, s,
+                           (const __bf16*)qkv, d, T_len, pos0, (__bf16*)kv, seq_stride);
     return hipGetLastError();
 }
 

@@ -84,6 +84,7 @@ bool config_ok(const pb_config* c, std::string* why) {
     if (c->max_adapters < 0 || c->max_adapters > MAX_SLOTS) return bad("max_adapters must be in [0, 16]");
     if (c->max_adapters > 0 && (c->max_rank < 1 || c->max_rank > MAX_RANK))
         return bad("max_rank must be in [1, 64]");
+    if (c->max_new_tokens < 0) return bad("max_new_tokens must be >= 0");
     if (c->dtype != PB_BF16 && c->dtype != PB_F16) return bad("dtype must be PB_BF16 or PB_F16");
     if (!(c->ln_eps > 0.f)) return bad("ln_eps must be > 0");
     return true;
@@ -160,6 +161,7 @@ struct ArenaLayout {
     int rs, kw;  // LoRA slot width (rank rounded up to 8) and packed width (multiple of 64)
     size_t globals, layers, layer_bytes, loraA, loraB, loraA_layer, loraB_layer;
     size_t x, u, qkv, attn, h, z, rowslot, tokens, slotscale, zf, logits, outtok, staging, ws;
+    size_t kv, kv_layer, kv_seq, dec_part;  // KV cache (elements per layer, per sequence) and decode scratch
     size_t pval, pidx;
     size_t staging_bytes, ws_bytes, total;
 };
@@ -200,6 +202,13 @@ ArenaLayout arena_layout(const pb_config* c) {
     a.pidx = take(B * (size_t)pb::lm_head_blocks((int)V) * 4);
     a.staging_bytes = c->max_adapters > 0 ? L * lora_layer_elems(c, c->max_rank, 0xF) * 2 : 0;
     a.staging = take(a.staging_bytes);
+    // KV cache for decoding: [L][max_batch][max_pos][k | v] (dt)
+    a.kv_seq = c->max_new_tokens > 0 ? (size_t)c->max_pos * 2 * d : 0;
+    a.kv_layer = (size_t)B * a.kv_seq;
+    a.kv = take(L * a.kv_layer * 2);
+    a.dec_part = take(c->max_new_tokens > 0
+                          ? pb::decode_attention_part_floats((int)B, c->n_heads, (int)(d / c->n_heads), c->max_pos) * 4
+                          : 0);
     a.ws_bytes = gemm_ws_bytes(c);
     a.ws = take(a.ws_bytes);
     a.total = align_up(p, ALIGN);
@@ -250,6 +259,9 @@ struct pb_model {
     hipEvent_t ring_ev[STAGE_SLOTS] = {};
     bool ring_busy[STAGE_SLOTS] = {};
     int ring_next = 0;
+    // decode state: sequences of the last prefill, their length so far
+    int dec_B = 0, dec_len = 0, dec_steps = 0;
+    std::vector<int> dec_adapter;
     size_t chunk_bytes = 256u << 20;
     int delay_us = 0;
     // adapter slots
@@ -636,6 +648,7 @@ int pb_poison_weights(pb_model* m, int32_t value) {
     if (end > a.loraA) HIP_TRY(hipMemsetAsync(m->at(a.loraA), 0, end - a.loraA, m->copy));
     for (int s = 0; s < MAX_SLOTS; ++s) m->slot_valid[s] = false;
     m->streamed = false;
+    m->dec_B = 0;
     return PB_OK;
 }
 
@@ -702,7 +715,12 @@ struct Timed {
     }
 };
 
-int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_union) {
+// The forward pass of B sequences of T new tokens at positions pos0 ..
+// pos0+T-1.  A prefill (decode = false) attends among its own tokens; a decode
+// step (T = 1) attends to the KV cache, which both append to when the model
+// keeps one.
+int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_union, int pos0 = 0,
+                    bool decode = false) {
     const pb_config& c = m->cfg;
     const ArenaLayout& a = m->lay;
     const int dt = c.dtype;
@@ -726,7 +744,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
     {
         Timed t(m, PB_K_EMBED);
         HIP_TRY(pb::launch_embed(dt, (const int32_t*)m->at(a.tokens), m->gtensor(PB_G_EMBED),
-                                 m->gtensor(PB_G_POS), x, N, T, d, s));
+                                 m->gtensor(PB_G_POS), x, N, T, d, s, pos0));
     }
     const bool qkv_lora = use_lora && (lora_union & (PB_LORA_Q | PB_LORA_K | PB_LORA_V));
     const bool o_lora = use_lora && (lora_union & PB_LORA_O);
@@ -776,9 +794,19 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             p.qscale = 1.0f / std::sqrt((float)hd); p.qcols = d;
             HIP_TRY(pb::launch_gemm(dt, 0, pb::EPI_QKV, p, gws, s));
         }
+        if (a.kv_layer) {  // keys and values of the new tokens into the cache
+            char* kvl = m->at(a.kv) + (size_t)l * a.kv_layer * 2;
+            HIP_TRY(pb::launch_kv_store(dt, qkv, N, T, pos0, d, kvl, (int64_t)a.kv_seq, s));
+        }
         {
             Timed t(m, PB_K_ATTN);
-            HIP_TRY(pb::launch_attention(dt, qkv, attn, B, T, H, hd, s));
+            if (!decode) {
+                HIP_TRY(pb::launch_attention(dt, qkv, attn, B, T, H, hd, s));
+            } else {
+                const char* kvl = m->at(a.kv) + (size_t)l * a.kv_layer * 2;
+                HIP_TRY(pb::launch_decode_attention(dt, qkv, kvl, (int64_t)a.kv_seq, B, H, hd, pos0 + 1,
+                                                    (float*)m->at(a.dec_part), attn, s));
+            }
         }
         if (o_lora) {
             Timed t(m, PB_K_LORA_SHRINK);
@@ -856,16 +884,12 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
 
 }  // namespace
 
-extern "C" int pb_prefill_first_token(pb_model* m, const int32_t* tokens, int32_t B, int32_t T,
-                                      const int32_t* adapter_of_seq, int32_t* out_tokens,
-                                      float* out_logits) {
-    if (!m) return fail(PB_EINVAL, "model is NULL");
+// Validate, stage the small inputs, enqueue the forward pass and return the
+// greedy tokens (and logits) of B sequences of T new tokens at position pos0.
+static int run_forward(pb_model* m, const int32_t* tokens, int32_t B, int32_t T,
+                       const int32_t* adapter_of_seq, int32_t* out_tokens, float* out_logits, int pos0,
+                       bool decode) {
     const pb_config& c = m->cfg;
-    if (!tokens || !out_tokens) return fail(PB_EINVAL, "tokens and out_tokens must be non-NULL");
-    if (B < 1 || B > c.max_batch) return fail(PB_EINVAL, "B=%d outside [1, %d]", B, c.max_batch);
-    if (T < 1 || T > c.max_pos) return fail(PB_EINVAL, "T=%d outside [1, %d]", T, c.max_pos);
-    if ((int64_t)B * T > c.max_tokens) return fail(PB_EINVAL, "B*T=%lld exceeds max_tokens=%d", (long long)B * T, c.max_tokens);
-    if (!m->streamed) return fail(PB_ESTATE, "prefill before pb_stream_layers");
     const int N = B * T;
     for (int i = 0; i < N; ++i)
         if (tokens[i] < 0 || tokens[i] >= c.vocab) return fail(PB_EINVAL, "token %d at %d outside [0, %d)", tokens[i], i, c.vocab);
@@ -889,7 +913,7 @@ extern "C" int pb_prefill_first_token(pb_model* m, const int32_t* tokens, int32_
     HIP_TRY(hipMemcpyAsync(m->at(a.tokens), m->h_tokens, (size_t)N * 4, hipMemcpyHostToDevice, s));
     HIP_TRY(hipMemcpyAsync(m->at(a.rowslot), m->h_rowslot, (size_t)N * 4, hipMemcpyHostToDevice, s));
     HIP_TRY(hipMemcpyAsync(m->at(a.slotscale), m->h_scale, MAX_SLOTS * 4, hipMemcpyHostToDevice, s));
-    int rc = enqueue_forward(m, B, T, use_lora, lora_union);
+    int rc = enqueue_forward(m, B, T, use_lora, lora_union, pos0, decode);
     if (rc) {
         (void)hipStreamSynchronize(s);
         return rc;
@@ -909,6 +933,50 @@ extern "C" int pb_prefill_first_token(pb_model* m, const int32_t* tokens, int32_
             m->tcount[k] += 1;
         }
     }
+    return PB_OK;
+}
+
+extern "C" int pb_prefill_first_token(pb_model* m, const int32_t* tokens, int32_t B, int32_t T,
+                                      const int32_t* adapter_of_seq, int32_t* out_tokens,
+                                      float* out_logits) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    const pb_config& c = m->cfg;
+    if (!tokens || !out_tokens) return fail(PB_EINVAL, "tokens and out_tokens must be non-NULL");
+    if (B < 1 || B > c.max_batch) return fail(PB_EINVAL, "B=%d outside [1, %d]", B, c.max_batch);
+    if (T < 1 || T > c.max_pos) return fail(PB_EINVAL, "T=%d outside [1, %d]", T, c.max_pos);
+    if ((int64_t)B * T > c.max_tokens) return fail(PB_EINVAL, "B*T=%lld exceeds max_tokens=%d", (long long)B * T, c.max_tokens);
+    if (!m->streamed) return fail(PB_ESTATE, "prefill before pb_stream_layers");
+    m->dec_B = 0;  // a failed prefill leaves nothing to decode from
+    const int rc = run_forward(m, tokens, B, T, adapter_of_seq, out_tokens, out_logits, 0, false);
+    if (rc) return rc;
+    if (c.max_new_tokens > 0) {
+        m->dec_B = B;
+        m->dec_len = T;
+        m->dec_steps = 0;
+        m->dec_adapter.assign(B, -1);
+        for (int b = 0; b < B; ++b) m->dec_adapter[b] = adapter_of_seq ? adapter_of_seq[b] : -1;
+    }
+    return PB_OK;
+}
+
+extern "C" int pb_decode_step(pb_model* m, const int32_t* tokens, int32_t B, const int32_t* adapter_of_seq,
+                              int32_t* out_tokens, float* out_logits) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    const pb_config& c = m->cfg;
+    if (!tokens || !out_tokens) return fail(PB_EINVAL, "tokens and out_tokens must be non-NULL");
+    if (c.max_new_tokens <= 0) return fail(PB_ESTATE, "the model was created without a KV cache (max_new_tokens = 0)");
+    if (m->dec_B == 0) return fail(PB_ESTATE, "decode step without a prefill to continue");
+    if (B != m->dec_B) return fail(PB_EINVAL, "B=%d differs from the prefill's %d sequences", B, m->dec_B);
+    for (int b = 0; b < B; ++b) {
+        const int a = adapter_of_seq ? adapter_of_seq[b] : -1;
+        if (a != m->dec_adapter[b]) return fail(PB_EINVAL, "sequence %d changed adapter since its prefill", b);
+    }
+    if (m->dec_steps >= c.max_new_tokens) return fail(PB_ESTATE, "max_new_tokens=%d reached", c.max_new_tokens);
+    if (m->dec_len >= c.max_pos) return fail(PB_ESTATE, "sequences already hold max_pos=%d tokens", c.max_pos);
+    const int rc = run_forward(m, tokens, B, 1, adapter_of_seq, out_tokens, out_logits, m->dec_len, true);
+    if (rc) return rc;
+    m->dec_len += 1;
+    m->dec_steps += 1;
     return PB_OK;
 }
 

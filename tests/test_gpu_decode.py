@@ -1,0 +1,122 @@
+"""Decode steps with the KV cache against the oracle: the greedy token and the
+logits of step k are those of a plain prefill over the prompt plus the k
+tokens generated so far (the decode stage of Section 2.1 computes exactly
+that, reusing the cached keys and values)."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_common import compare, log
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    # three sequences, adapters 0 / none / 1 on q, k, v, o, f16, head_dim 64
+    "mixed": synth.Workload(name="mixed", seed=31, n_layers=2, d_model=256, n_heads=4, d_ffn=512,
+                            vocab=1000, max_pos=128, dtype="f16", batch=3, seq_len=37,
+                            lora_targets=("q", "k", "v", "o"), lora_rank=8, lora_alpha=16.0,
+                            n_adapters=2, adapter_of_seq=(0, -1, 1)),
+    # bf16, head_dim 128, a prompt long enough for several key splits of 256
+    "hd128": synth.Workload(name="hd128", seed=32, n_layers=2, d_model=256, n_heads=2, d_ffn=384,
+                            vocab=777, max_pos=640, dtype="bf16", batch=2, seq_len=300,
+                            lora_targets=("q", "v"), lora_rank=16, lora_alpha=32.0, n_adapters=1),
+}
+STEPS = 4
+
+
+def _model(w, new_tokens):
+    from paper_2503_17707_amd import binding as pb
+
+    cfg = pb.make_config(w, max_new_tokens=new_tokens)
+    hw = pb.HostWeights(w, cfg)
+    m = pb.Model(cfg, "cuda:0")
+    pb.attach_all(m, hw)
+    m.stream_layers(hw, w.order())
+    return hw, m
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_decode_steps_match_oracle_prefill_of_extended_prompt(name):
+    w = CASES[name]
+    log("case decode", name)
+    hw, m = _model(w, STEPS)
+    try:
+        ad = list(w.adapters())
+        seq = synth.tokens(w).astype(np.int32)
+        tok, logits = m.prefill(seq, ad)
+        for step in range(STEPS):
+            seq = np.concatenate([seq, tok[:, None]], axis=1)
+            tok, logits = m.decode(tok, ad)
+            ref_logits, ref_tok = oracle.prefill_first_token(w, tokens=seq, adapter_of_seq=ad)
+            compare("%s decode step %d (T=%d)" % (name, step + 1, seq.shape[1]), logits, tok,
+                    ref_logits, ref_tok)
+    finally:
+        m.destroy()
+        hw.free()
+
+
+def test_decode_equals_gpu_prefill_of_extended_prompt():
+    """The cached path and a fresh prefill over the longer prompt agree to
+    rounding (different reduction orders only)."""
+    w = CASES["mixed"]
+    hw, m = _model(w, 2)
+    try:
+        ad = list(w.adapters())
+        seq = synth.tokens(w).astype(np.int32)
+        tok, _ = m.prefill(seq, ad)
+        tok2, dec_logits = m.decode(tok, ad)
+        ext = np.concatenate([seq, tok[:, None]], axis=1)
+        w2 = w.with_(seq_len=ext.shape[1])
+        from paper_2503_17707_amd import binding as pb
+        hw2, m2 = pb.setup(w2)
+        try:
+            pb.attach_all(m2, hw2)
+            m2.stream_layers(hw2)
+            tok_p, pre_logits = m2.prefill(ext, ad)
+        finally:
+            m2.destroy()
+            hw2.free()
+        log("  decode vs prefill max|d| %.2e" % float(np.max(np.abs(dec_logits - pre_logits))))
+        assert np.array_equal(tok2, tok_p)
+        assert float(np.max(np.abs(dec_logits - pre_logits))) <= 2e-2
+    finally:
+        m.destroy()
+        hw.free()
+
+
+def test_decode_state_errors():
+    from paper_2503_17707_amd import binding as pb
+
+    w = CASES["mixed"]
+    ad = list(w.adapters())
+    seq = synth.tokens(w).astype(np.int32)
+    # no KV cache in the config
+    hw, m = _model(w, 0)
+    try:
+        tok, _ = m.prefill(seq, ad)
+        with pytest.raises(pb.PbError) as e:
+            m.decode(tok, ad)
+        assert e.value.code == pb.PB_ESTATE
+    finally:
+        m.destroy()
+        hw.free()
+    hw, m = _model(w, 1)
+    try:
+        with pytest.raises(pb.PbError) as e:  # nothing to continue yet
+            m.decode(seq[:, 0], ad)
+        assert e.value.code == pb.PB_ESTATE
+        tok, _ = m.prefill(seq, ad)
+        with pytest.raises(pb.PbError) as e:  # another batch size
+            m.decode(tok[:2], ad[:2])
+        assert e.value.code == pb.PB_EINVAL
+        with pytest.raises(pb.PbError) as e:  # another adapter
+            m.decode(tok, [1, -1, 1])
+        assert e.value.code == pb.PB_EINVAL
+        tok, _ = m.decode(tok, ad)
+        with pytest.raises(pb.PbError) as e:  # max_new_tokens = 1 reached
+            m.decode(tok, ad)
+        assert e.value.code == pb.PB_ESTATE
+    finally:
+        m.destroy()
+        hw.free()
