@@ -12,6 +12,9 @@ B=1, T=512, LoRA rank 16 on q and v, fp16 weights, random init) is synthetic.
 * roofline: the dominant kernel's average duration from per-kernel HIP events
   on the compute stream (a separate pass of the same K steps), against the
   dense fp16 MFMA peak.
+* decode: greedy decode steps with the KV cache after a prefill (ms per step,
+  weight bytes read per second against HBM), checked against the oracle's
+  stored decode logits when present.
 * cpu_baseline: the CPU oracle timed on a bounded sample of the same workload.
 """
 import argparse
@@ -206,6 +209,8 @@ def main():
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (3 times) and exit: "
                          "the reference kernel for scaling HBM byte counters")
+    ap.add_argument("--decode-steps", type=int, default=32,
+                    help="greedy decode steps timed after the prefill (0 = none)")
     ap.add_argument("--h2d-sweep", action="store_true",
                     help="only measure the loader's H2D rate over chunk sizes, and plain pinned "
                          "copies on one and two streams, then exit")
@@ -239,7 +244,9 @@ def main():
         return
     dev = torch.device("cuda:0")
     t0 = time.perf_counter()
-    cfg = pb.make_config(w)
+    # room for decode steps after the prompt (none when the prompt fills max_pos)
+    dec_steps = max(0, min(args.decode_steps, w.max_pos - w.seq_len))
+    cfg = pb.make_config(w, max_new_tokens=dec_steps)
     hw = pb.HostWeights(w, cfg)
     for a in sorted({a for a in w.adapters() if a >= 0}):
         hw.add_lora(a)
@@ -319,6 +326,39 @@ def main():
         m.prefill(toks, ad)
     m.set_timing(False)
     kt = m.timing()
+
+    # ---- decode: greedy steps with the KV cache after a prefill -----------
+    decode = None
+    if dec_steps:
+        gd = os.path.join(ROOT, "tests", "golden", w.name + "-decode.npz")
+        tok, _ = m.prefill(toks, ad)
+        dec_parity = None
+        if os.path.exists(gd):
+            g = np.load(gd, allow_pickle=False)
+            k = min(dec_steps, g["tokens"].shape[0])
+            t_ok, worst, rel = True, 0.0, 0.0
+            cur = tok
+            for i in range(k):
+                cur, lg = m.decode(cur, ad)
+                ref = g["logits"][i].astype(np.float64)
+                t_ok &= bool(np.array_equal(cur, g["tokens"][i]))
+                worst = max(worst, float(np.max(np.abs(lg - ref))))
+                rel = max(rel, float(np.linalg.norm(lg - ref) / np.linalg.norm(ref)))
+            dec_parity = {"steps": k, "tokens_equal": t_ok, "max_abs": worst, "rel_l2": rel}
+            tok, _ = m.prefill(toks, ad)
+        torch.cuda.synchronize(dev)
+        t0 = time.perf_counter()
+        cur = tok
+        for _ in range(dec_steps):
+            cur, _ = m.decode(cur, ad, want_logits=False)
+        dt_dec = time.perf_counter() - t0
+        ms_tok = dt_dec / dec_steps * 1e3
+        wbytes = h2d_bytes + lora_bytes  # every step reads every weight once
+        decode = {"steps": dec_steps, "ms_per_step": ms_tok,
+                  "tokens_per_s": w.batch * dec_steps / dt_dec,
+                  "weight_GBps": wbytes / (ms_tok / 1e3) / 1e9,
+                  "frac_of_hbm": wbytes / (ms_tok / 1e3) / 1e9 / HBM_PEAK_GBPS,
+                  "parity": dec_parity}
     kernels = {k: {"avg_ms": (v[0] / v[1]) if v[1] else None, "launches_per_step": v[1] / args.steps,
                    "ms_per_step": v[0] / args.steps} for k, v in kt.items()}
     cand = [k for k in kt if kernel_flops(w, k) is not None and kt[k][1]]
@@ -371,6 +411,7 @@ def main():
         "h2d": {"GBps": b_meas, "frac_of_pcie_gen5_x16": b_meas / PCIE5_X16_GBPS},
         "roofline": roofline,
         "kernels": kernels,
+        "decode": decode,
         "parity": parity,
         "cpu_baseline": cpu,
     }

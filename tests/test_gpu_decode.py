@@ -120,3 +120,31 @@ def test_decode_state_errors():
     finally:
         m.destroy()
         hw.free()
+
+
+def test_opt_1_3b_decode_matches_stored_oracle_steps():
+    """OPT-1.3B workload: two greedy decode steps after the cold-start prefill
+    against the oracle's stored logits of those steps (make_golden.py --decode)."""
+    import os
+
+    from gpu_common import golden_path
+
+    name = "opt-1.3b"
+    p = golden_path(name + "-decode")
+    if not os.path.exists(p):
+        pytest.skip("oracle decode logits for %s not generated" % name)
+    g = np.load(p, allow_pickle=False)
+    w = synth.WORKLOADS[name]
+    k = g["tokens"].shape[0]
+    log("case decode", name, "steps", k)
+    hw, m = _model(w, k)
+    try:
+        ad = list(w.adapters())
+        tok, _ = m.prefill(synth.tokens(w), ad)
+        for i in range(k):
+            tok, logits = m.decode(tok, ad)
+            compare("%s decode step %d" % (name, i + 1), logits, tok, g["logits"][i].astype(np.float64),
+                    g["tokens"][i])
+    finally:
+        m.destroy()
+        hw.free()
