@@ -189,6 +189,24 @@ int pb_prefill_first_token(pb_model* m, const int32_t* tokens, int32_t B, int32_
 int pb_decode_step(pb_model* m, const int32_t* tokens, int32_t B, const int32_t* adapter_of_seq,
                    int32_t* out_tokens, float* out_logits);
 
+/* KV-cache reconstruction after a failure (Section 4.4.2: a request that was
+ * decoding is replayed as one prefill over its prompt and the tokens produced
+ * so far).  tokens: host int32 [B*T], sequence-major.  For every layer l with
+ * layer_has_kv[l] != 0 the cache still holds keys and values of positions
+ * 0..T-1: that layer computes only the queries and attends to the cache; the
+ * other layers run a full prefill and store their keys and values.  Returns
+ * the next greedy token (and optional logits) of each sequence, like the decode
+ * step that would have come next, and leaves the model ready to continue with
+ * pb_decode_step.  Requires max_new_tokens > 0 and the prefill's limits. */
+int pb_rebuild_kv(pb_model* m, const int32_t* tokens, int32_t B, int32_t T, const int32_t* adapter_of_seq,
+                  const uint8_t* layer_has_kv, int32_t* out_tokens, float* out_logits);
+
+/* Overwrite the KV cache of every layer l with layer_lost[l] != 0 with the
+ * byte `value` (0xFF: NaN), on the compute stream, and wait for it.  For
+ * failure-recovery tests: the cache those layers held is gone, and any read of
+ * it before a rebuild shows up as NaN. */
+int pb_invalidate_kv(pb_model* m, const uint8_t* layer_lost, int32_t value);
+
 /* Release the model's events and staging (not the caller's arena or streams). */
 int pb_destroy(pb_model* m);
 

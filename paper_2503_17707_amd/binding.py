@@ -71,6 +71,11 @@ _SIGS = {
     "pb_attach_lora": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                       ctypes.c_float, ctypes.c_uint32,
                                       ctypes.POINTER(ctypes.c_void_p)]),
+    "pb_rebuild_kv": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
+                                     ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
+                                     ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(ctypes.c_int32),
+                                     ctypes.POINTER(ctypes.c_float)]),
+    "pb_invalidate_kv": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_uint8), ctypes.c_int32]),
     "pb_decode_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
                                       ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
                                       ctypes.POINTER(ctypes.c_float)]),
@@ -362,6 +367,29 @@ class Model:
             out_tok.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
             logits.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if want_logits else None))
         return out_tok, logits
+
+    def rebuild_kv(self, tokens: np.ndarray, layer_has_kv: Sequence[bool],
+                   adapter_of_seq: Optional[Sequence[int]] = None, want_logits: bool = True):
+        """KV-cache rebuild over tokens [B, T]; returns the next token of each sequence."""
+        tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+        B, T = tokens.shape
+        has = np.ascontiguousarray([1 if h else 0 for h in layer_has_kv], dtype=np.uint8)
+        out_tok = np.empty(B, dtype=np.int32)
+        logits = np.empty((B, self.cfg.vocab), dtype=np.float32) if want_logits else None
+        ad = None
+        if adapter_of_seq is not None:
+            ad_arr = np.ascontiguousarray(adapter_of_seq, dtype=np.int32)
+            ad = ad_arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        check(lib().pb_rebuild_kv(
+            self.h, tokens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), B, T, ad,
+            has.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)),
+            out_tok.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+            logits.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if want_logits else None))
+        return out_tok, logits
+
+    def invalidate_kv(self, layer_lost: Sequence[bool], value: int = 0xFF):
+        lost = np.ascontiguousarray([1 if x else 0 for x in layer_lost], dtype=np.uint8)
+        check(lib().pb_invalidate_kv(self.h, lost.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), value))
 
     def poison(self, value: int = 0xFF):
         check(lib().pb_poison_weights(self.h, value))

@@ -60,8 +60,8 @@ __device__ __forceinline__ u32x2 read_tr16(const uint8_t* p) {
 
 template <typename T, int HD, int QW>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(QW == 32 ? 2 : 1)))
-void attention_kernel(const T* __restrict__ qkv,
-                                                       T* __restrict__ out, int T_len, int H) {
+void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, int64_t kv_ld, int64_t kv_seq,
+                      T* __restrict__ out, int T_len, int H) {
     typedef typename Mfma<T>::vec8 vec8;
     constexpr int BQ = 4 * QW;         // queries per block (4 waves)
     constexpr int NQG = QW / 16;       // 16-query groups per wave
@@ -111,7 +111,7 @@ void attention_kernel(const T* __restrict__ qkv,
             const int pch = lane % CPR;
             const int ch = isv ? vswz<HD>(row, pch) : kswz(row, pch);
             const int key = min(kb * BKV + row, T_len - 1);
-            const T* src = qkv + (row0 + key) * ld + (isv ? 2 * d : d) + h * HD + ch * 8;
+            const T* src = kvsrc + b * kv_seq + key * kv_ld + (isv ? d : 0) + h * HD + ch * 8;
             dma16(src, sbase + (uint32_t)__builtin_amdgcn_readfirstlane(I * 1024));
         }
     };
@@ -261,7 +261,8 @@ void attention_kernel(const T* __restrict__ qkv,
 }
 
 template <typename T, int HD, int QW>
-hipError_t launch_hd(const void* qkv, void* out, int B, int T_len, int H, hipStream_t s) {
+hipError_t launch_hd(const void* qkv, const void* kv, int64_t kv_ld, int64_t kv_seq, void* out, int B,
+                     int T_len, int H, hipStream_t s) {
     constexpr int LDS = 2 * 2 * BKV * HD * 2;
     static bool attr_set = false;
     if (!attr_set) {
@@ -271,19 +272,19 @@ hipError_t launch_hd(const void* qkv, void* out, int B, int T_len, int H, hipStr
         attr_set = true;
     }
     dim3 grid((T_len + 4 * QW - 1) / (4 * QW), H, B);
-    hipLaunchKernelGGL((attention_kernel<T, HD, QW>), grid, dim3(256), LDS, s, (const T*)qkv,
-                       (T*)out, T_len, H);
+    hipLaunchKernelGGL((attention_kernel<T, HD, QW>), grid, dim3(256), LDS, s, (const T*)qkv, (const T*)kv,
+                       kv_ld, kv_seq, (T*)out, T_len, H);
     return hipGetLastError();
 }
 
 template <typename T, int HD>
-hipError_t launch_qw(const void* qkv, void* out, int B, int T_len, int H, hipStream_t s) {
+hipError_t launch_qw(const void* qkv, const void* kv, int64_t kv_ld, int64_t kv_seq, void* out, int B,
+                     int T_len, int H, hipStream_t s) {
     // 32 queries per wave when 128-query blocks still give every CU work
     const long blocks128 = (long)((T_len + 127) / 128) * H * B;
-    if (PB_ATTN_QW32 && blocks128 >= 512) return launch_hd<T, HD, 32>(qkv, out, B, T_len, H, s);
-    return launch_hd<T, HD, 16>(qkv, out, B, T_len, H, s);
+    if (PB_ATTN_QW32 && blocks128 >= 512) return launch_hd<T, HD, 32>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
+    return launch_hd<T, HD, 16>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
 }
-
 
 // ---- decode: one new query per (sequence, head) against the KV cache --------
 // Split over keys (256 per block, 64 per wave): each lane scores one key
@@ -399,18 +400,27 @@ hipError_t launch_decode_hd(const void* qkv, const void* kv, int64_t seq_stride,
 }
 }  // namespace
 
-hipError_t launch_attention(int dtype, const void* qkv, void* out, int B, int T_len, int H,
-                            int hd, hipStream_t s) {
+hipError_t launch_attention_kv(int dtype, const void* qkv, const void* kv, int64_t kv_ld, int64_t kv_seq,
+                               void* out, int B, int T_len, int H, int hd, hipStream_t s) {
     if (B <= 0 || T_len <= 0) return hipSuccess;
-    if ((int64_t)B * T_len * 3 * H * hd >= ((int64_t)1 << 31)) return hipErrorInvalidValue;
+    if ((int64_t)B * T_len * 3 * H * hd >= ((int64_t)1 << 31) || (int64_t)B * kv_seq >= ((int64_t)1 << 31))
+        return hipErrorInvalidValue;
     if (dtype == 1) {
-        if (hd == 64) return launch_qw<_Float16, 64>(qkv, out, B, T_len, H, s);
-        if (hd == 128) return launch_qw<_Float16, 128>(qkv, out, B, T_len, H, s);
+        if (hd == 64) return launch_qw<_Float16, 64>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
+        if (hd == 128) return launch_qw<_Float16, 128>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
     } else {
-        if (hd == 64) return launch_qw<__bf16, 64>(qkv, out, B, T_len, H, s);
-        if (hd == 128) return launch_qw<__bf16, 128>(qkv, out, B, T_len, H, s);
+        if (hd == 64) return launch_qw<__bf16, 64>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
+        if (hd == 128) return launch_qw<__bf16, 128>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
     }
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_attention(int dtype, const void* qkv, void* out, int B, int T_len, int H, int hd,
+                            hipStream_t s) {
+    // keys and values from the same rows: K at column d, V at 2d, 3d per row
+    const int64_t d = (int64_t)H * hd;
+    return launch_attention_kv(dtype, qkv, (const char*)qkv + d * 2, 3 * d, (int64_t)T_len * 3 * d, out, B,
+                               T_len, H, hd, s);
 }
 
 size_t decode_attention_part_floats(int B, int H, int hd, int max_keys) {

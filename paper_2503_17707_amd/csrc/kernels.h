@@ -59,6 +59,10 @@ hipError_t launch_gemm(int dtype, int role, int epi, const GemmParams& p, const 
 // qkv: [B*T, 3d] (q already divided by sqrt(head_dim)); out: [B*T, d].
 hipError_t launch_attention(int dtype, const void* qkv, void* out, int B, int T, int H, int hd,
                             hipStream_t s);
+// The same with keys and values elsewhere: key of (sequence b, position t) at
+// kv + b * kv_seq + t * kv_ld (+ h * hd), its value d elements further.
+hipError_t launch_attention_kv(int dtype, const void* qkv, const void* kv, int64_t kv_ld, int64_t kv_seq,
+                               void* out, int B, int T, int H, int hd, hipStream_t s);
 
 // x[b*T + t, :] = E[tok[b*T + t], :] + P[t, :] (fp32 output).
 hipError_t launch_embed(int dtype, const int32_t* tok, const void* E, const void* P, float* x,

@@ -720,7 +720,7 @@ struct Timed {
 // step (T = 1) attends to the KV cache, which both append to when the model
 // keeps one.
 int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_union, int pos0 = 0,
-                    bool decode = false) {
+                    bool decode = false, const uint8_t* has_kv = nullptr) {
     const pb_config& c = m->cfg;
     const ArenaLayout& a = m->lay;
     const int dt = c.dtype;
@@ -781,26 +781,34 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             p.row_slot = rowslot; p.slot_scale = sscale; p.slot_width = a.rs; p.kw = kw;
             HIP_TRY(pb::launch_gemm(dt, 4, pb::EPI_SHRINK, p, gws, s));
         }
+        // a layer whose cache already holds keys and values for every position
+        // (KV rebuild) computes only the queries and attends to the cache
+        const bool reuse_kv = has_kv && has_kv[l];
         {
             Timed t(m, PB_K_GEMM_QKV);
             pb::GemmParams p{};
-            p.X = u; p.ldx = d; p.W = m->ltensor(l, PB_T_WQ); p.ldw = d; p.M = N; p.N = 3 * d; p.K1 = d;
-            if (qkv_lora) {
+            p.X = u; p.ldx = d; p.W = m->ltensor(l, PB_T_WQ); p.ldw = d; p.M = N; p.N = (reuse_kv ? 1 : 3) * d;
+            p.K1 = d;
+            if (qkv_lora && (!reuse_kv || (lora_union & PB_LORA_Q))) {
                 p.X2 = z; p.ldx2 = 4 * kw; p.W2 = Bq; p.ldw2 = kw; p.K2 = kw; p.group = d;
-                p.k2_mask = lora_union & 7u; p.x2_group_stride = kw;
+                p.k2_mask = lora_union & (reuse_kv ? 1u : 7u); p.x2_group_stride = kw;
             }
             p.bias = m->ltensor(l, PB_T_BQ);
             p.C = qkv; p.ldc = 3 * d;
             p.qscale = 1.0f / std::sqrt((float)hd); p.qcols = d;
             HIP_TRY(pb::launch_gemm(dt, 0, pb::EPI_QKV, p, gws, s));
         }
-        if (a.kv_layer) {  // keys and values of the new tokens into the cache
+        if (a.kv_layer && !reuse_kv) {  // keys and values of the new tokens into the cache
             char* kvl = m->at(a.kv) + (size_t)l * a.kv_layer * 2;
             HIP_TRY(pb::launch_kv_store(dt, qkv, N, T, pos0, d, kvl, (int64_t)a.kv_seq, s));
         }
         {
             Timed t(m, PB_K_ATTN);
-            if (!decode) {
+            if (reuse_kv) {
+                const char* kvl = m->at(a.kv) + (size_t)l * a.kv_layer * 2;
+                HIP_TRY(pb::launch_attention_kv(dt, qkv, kvl, 2 * (int64_t)d, (int64_t)a.kv_seq, attn, B, T, H,
+                                                hd, s));
+            } else if (!decode) {
                 HIP_TRY(pb::launch_attention(dt, qkv, attn, B, T, H, hd, s));
             } else {
                 const char* kvl = m->at(a.kv) + (size_t)l * a.kv_layer * 2;
@@ -888,7 +896,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
 // greedy tokens (and logits) of B sequences of T new tokens at position pos0.
 static int run_forward(pb_model* m, const int32_t* tokens, int32_t B, int32_t T,
                        const int32_t* adapter_of_seq, int32_t* out_tokens, float* out_logits, int pos0,
-                       bool decode) {
+                       bool decode, const uint8_t* has_kv = nullptr) {
     const pb_config& c = m->cfg;
     const int N = B * T;
     for (int i = 0; i < N; ++i)
@@ -913,7 +921,7 @@ static int run_forward(pb_model* m, const int32_t* tokens, int32_t B, int32_t T,
     HIP_TRY(hipMemcpyAsync(m->at(a.tokens), m->h_tokens, (size_t)N * 4, hipMemcpyHostToDevice, s));
     HIP_TRY(hipMemcpyAsync(m->at(a.rowslot), m->h_rowslot, (size_t)N * 4, hipMemcpyHostToDevice, s));
     HIP_TRY(hipMemcpyAsync(m->at(a.slotscale), m->h_scale, MAX_SLOTS * 4, hipMemcpyHostToDevice, s));
-    int rc = enqueue_forward(m, B, T, use_lora, lora_union, pos0, decode);
+    int rc = enqueue_forward(m, B, T, use_lora, lora_union, pos0, decode, has_kv);
     if (rc) {
         (void)hipStreamSynchronize(s);
         return rc;
@@ -977,6 +985,41 @@ extern "C" int pb_decode_step(pb_model* m, const int32_t* tokens, int32_t B, con
     if (rc) return rc;
     m->dec_len += 1;
     m->dec_steps += 1;
+    return PB_OK;
+}
+
+extern "C" int pb_rebuild_kv(pb_model* m, const int32_t* tokens, int32_t B, int32_t T,
+                             const int32_t* adapter_of_seq, const uint8_t* layer_has_kv,
+                             int32_t* out_tokens, float* out_logits) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    const pb_config& c = m->cfg;
+    if (!tokens || !out_tokens || !layer_has_kv) return fail(PB_EINVAL, "NULL argument");
+    if (c.max_new_tokens <= 0) return fail(PB_ESTATE, "the model was created without a KV cache (max_new_tokens = 0)");
+    if (B < 1 || B > c.max_batch) return fail(PB_EINVAL, "B=%d outside [1, %d]", B, c.max_batch);
+    if (T < 1 || T > c.max_pos) return fail(PB_EINVAL, "T=%d outside [1, %d]", T, c.max_pos);
+    if ((int64_t)B * T > c.max_tokens) return fail(PB_EINVAL, "B*T=%lld exceeds max_tokens=%d", (long long)B * T, c.max_tokens);
+    if (!m->streamed) return fail(PB_ESTATE, "rebuild before pb_stream_layers");
+    m->dec_B = 0;
+    const int rc = run_forward(m, tokens, B, T, adapter_of_seq, out_tokens, out_logits, 0, false, layer_has_kv);
+    if (rc) return rc;
+    m->dec_B = B;
+    m->dec_len = T;
+    m->dec_steps = 0;
+    m->dec_adapter.assign(B, -1);
+    for (int b = 0; b < B; ++b) m->dec_adapter[b] = adapter_of_seq ? adapter_of_seq[b] : -1;
+    return PB_OK;
+}
+
+extern "C" int pb_invalidate_kv(pb_model* m, const uint8_t* layer_lost, int32_t value) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    if (!layer_lost) return fail(PB_EINVAL, "layer_lost is NULL");
+    const ArenaLayout& a = m->lay;
+    if (!a.kv_layer) return fail(PB_ESTATE, "the model has no KV cache");
+    for (int l = 0; l < m->cfg.n_layers; ++l)
+        if (layer_lost[l])
+            HIP_TRY(hipMemsetAsync(m->at(a.kv) + (size_t)l * a.kv_layer * 2, value & 0xFF, a.kv_layer * 2,
+                                   m->compute));
+    HIP_TRY(hipStreamSynchronize(m->compute));
     return PB_OK;
 }
 

@@ -148,3 +148,42 @@ def test_opt_1_3b_decode_matches_stored_oracle_steps():
     finally:
         m.destroy()
         hw.free()
+
+
+@pytest.mark.parametrize("lost", [(0, 1, 0, 1), (1, 1, 1, 1)])
+def test_kv_rebuild_after_losing_layers(lost):
+    """Failure recovery (Section 4.4.2): after two decode steps the KV cache of
+    some layers is lost (NaN-filled).  A rebuild over the tokens processed so
+    far recomputes only the queries in the surviving layers and everything in
+    the lost ones; it reproduces the last decode output, and decoding then
+    continues as the oracle says."""
+    w = CASES["mixed"].with_(n_layers=4)
+    B, T = w.batch, w.seq_len
+    from paper_2503_17707_amd import binding as pb
+
+    log("case kv rebuild, lost layers", lost)
+    cfg = pb.make_config(w, max_new_tokens=4, max_tokens=B * (T + 4))
+    hw = pb.HostWeights(w, cfg)
+    m = pb.Model(cfg, "cuda:0")
+    try:
+        pb.attach_all(m, hw)
+        m.stream_layers(hw, w.order())
+        ad = list(w.adapters())
+        seq = synth.tokens(w).astype(np.int32)
+        t1, _ = m.prefill(seq, ad)
+        t2, _ = m.decode(t1, ad)
+        t3, _ = m.decode(t2, ad)
+        processed = np.concatenate([seq, t1[:, None], t2[:, None]], axis=1)
+        m.invalidate_kv([bool(x) for x in lost])
+        r3, lg3 = m.rebuild_kv(processed, [not x for x in lost], ad)
+        assert np.all(np.isfinite(lg3))
+        assert np.array_equal(r3, t3)
+        ref, ref_tok = oracle.prefill_first_token(w, tokens=processed, adapter_of_seq=ad)
+        compare("rebuild (T=%d)" % processed.shape[1], lg3, r3, ref, ref_tok)
+        t4, lg4 = m.decode(r3, ad)
+        ext = np.concatenate([processed, r3[:, None]], axis=1)
+        ref, ref_tok = oracle.prefill_first_token(w, tokens=ext, adapter_of_seq=ad)
+        compare("decode after rebuild (T=%d)" % ext.shape[1], lg4, t4, ref, ref_tok)
+    finally:
+        m.destroy()
+        hw.free()
