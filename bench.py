@@ -12,6 +12,8 @@ B=1, T=512, LoRA rank 16 on q and v, fp16 weights, random init) is synthetic.
 * roofline: the dominant kernel's average duration from per-kernel HIP events
   on the compute stream (a separate pass of the same K steps), against the
   dense fp16 MFMA peak.
+* merged_lora: the same prefill after folding the adapter into the base
+  weights (when the workload uses one adapter), against the unmerged time.
 * decode: greedy decode steps with the KV cache after a prefill (ms per step,
   weight bytes read per second against HBM), checked against the oracle's
   stored decode logits when present.
@@ -369,6 +371,28 @@ def main():
                 "unit": "TFLOP/s", "frac": achieved / MFMA_PEAK_TFLOPS,
                 "traffic": profiled_traffic(w.name, dom), "traffic_unit": "bytes per launch",
                 "avg_launch_ms": avg_ms, "flops_per_launch": kernel_flops(w, dom)}
+    # ---- merged LoRA (the paper's choice for pipeline inference): the adapter
+    # folded into the base weights, every sequence run as the base model ----
+    merged = None
+    used = sorted({a for a in ad if a >= 0})
+    if len(used) == 1:
+        t0 = time.perf_counter()
+        m.merge_lora(used[0])
+        merge_ms = (time.perf_counter() - t0) * 1e3
+        base_ad = [-1] * len(ad)
+        mt, ml = m.prefill(toks, base_ad)
+        for _ in range(args.warmup):
+            m.prefill(toks, base_ad)
+        torch.cuda.synchronize(dev)
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            m.prefill(toks, base_ad)
+        torch.cuda.synchronize(dev)
+        ms_m = (time.perf_counter() - t0) / args.steps * 1e3
+        merged = {"slot": used[0], "merge_ms": merge_ms, "ms_per_step": ms_m,
+                  "unmerged_over_merged": ms_step / ms_m,
+                  "tokens_equal_unmerged": bool(np.array_equal(mt, first[0])),
+                  "max_abs_vs_unmerged": float(np.max(np.abs(ml - first[1])))}
     m.destroy()
     hw.free()
 
@@ -412,6 +436,7 @@ def main():
         "roofline": roofline,
         "kernels": kernels,
         "decode": decode,
+        "merged_lora": merged,
         "parity": parity,
         "cpu_baseline": cpu,
     }

@@ -189,6 +189,16 @@ int pb_prefill_first_token(pb_model* m, const int32_t* tokens, int32_t B, int32_
 int pb_decode_step(pb_model* m, const int32_t* tokens, int32_t B, const int32_t* adapter_of_seq,
                    int32_t* out_tokens, float* out_logits);
 
+/* Merged LoRA (Section 4.3.2): fold adapter slot `slot` into the device base
+ * weights of every layer, W_t = dt(W_t + scale * B_t A_t) for each of its
+ * targets (fp32 product, one rounding), on the compute stream after every
+ * layer's copy; blocks until done.  Afterwards the base weights are the merged
+ * model: every sequence runs with adapter -1 (a prefill or decode naming any
+ * adapter fails with PB_ESTATE) and no LoRA work remains on the hot path.
+ * pb_stream_layers (or pb_poison_weights) restores the unmerged state.
+ * Requires an attached slot and a prior pb_stream_layers (PB_ESTATE). */
+int pb_merge_lora(pb_model* m, int32_t slot);
+
 /* KV-cache reconstruction after a failure (Section 4.4.2: a request that was
  * decoding is replayed as one prefill over its prompt and the tokens produced
  * so far).  tokens: host int32 [B*T], sequence-major.  For every layer l with

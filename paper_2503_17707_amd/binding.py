@@ -76,6 +76,7 @@ _SIGS = {
                                      ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(ctypes.c_int32),
                                      ctypes.POINTER(ctypes.c_float)]),
     "pb_invalidate_kv": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_uint8), ctypes.c_int32]),
+    "pb_merge_lora": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
     "pb_decode_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
                                       ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
                                       ctypes.POINTER(ctypes.c_float)]),
@@ -386,6 +387,9 @@ class Model:
             out_tok.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
             logits.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if want_logits else None))
         return out_tok, logits
+
+    def merge_lora(self, slot: int):
+        check(lib().pb_merge_lora(self.h, slot))
 
     def invalidate_kv(self, layer_lost: Sequence[bool], value: int = 0xFF):
         lost = np.ascontiguousarray([1 if x else 0 for x in layer_lost], dtype=np.uint8)

@@ -54,6 +54,9 @@ namespace {
 #ifndef PB_GEMM_S64
 #define PB_GEMM_S64 4  // ... of the 64 x 64 tiles
 #endif
+#ifndef PB_GEMM_GEMV
+#define PB_GEMM_GEMV 1  // weight-streaming kernel for at most 8 token rows
+#endif
 #ifndef PB_GEMM_S256
 #define PB_GEMM_S256 2  // ... of the 256 x 256 tiles
 #endif
@@ -492,6 +495,99 @@ hipError_t launch_typed(int role, const GemmParams& p, const GemmWorkspace& wsp,
     return hipErrorInvalidValue;
 }
 
+// ---- few rows (decode steps): weight streaming without tiles ---------------
+// Each wave owns four consecutive output features n0..n0+3 and walks K in
+// 512-element chunks (lane i takes elements 8i..8i+7 of a chunk, so a row's
+// chunk is one contiguous 1 KiB read), accumulating all MR token rows at once
+// (MR <= 8: the rows of X are re-read from cache by every wave); then the LoRA
+// K2 columns of the tile's group the same way, a wave sum per output, and lane
+// 0 applies the usual epilogue to the four features of each token.
+constexpr int GEMV_MAX_M = 8;
+
+template <typename T, int MR>
+__device__ __forceinline__ void gemv_dot(const T* __restrict__ X, int64_t ldx, const T* __restrict__ W,
+                                         int64_t ldw, int n0, int M, int K, int lane,
+                                         float (&acc)[4][MR]) {
+    for (int c0 = lane * 8; c0 < K; c0 += 2 * 512) {
+        u32x4 wr[2][4], xr[2][MR];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int c = min(c0 + u * 512, K - 8);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) wr[u][r] = *(const u32x4*)(W + (int64_t)(n0 + r) * ldw + c);
+#pragma unroll
+            for (int m = 0; m < MR; ++m) xr[u][m] = *(const u32x4*)(X + (int64_t)min(m, M - 1) * ldx + c);
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            if (c0 + u * 512 >= K) break;  // wave-uniform
+#pragma unroll
+            for (int m = 0; m < MR; ++m) {
+                T xe[8];
+                __builtin_memcpy(xe, &xr[u][m], 16);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    T we[8];
+                    __builtin_memcpy(we, &wr[u][r], 16);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) acc[r][m] += (float)we[e] * (float)xe[e];
+                }
+            }
+        }
+    }
+}
+
+template <typename T, int EPI, int MR>
+__global__ __launch_bounds__(256) void gemv_kernel(GemmParams p) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n0 = (blockIdx.x * 4 + wave) * 4;
+    if (n0 >= p.N) return;  // wave-uniform; no barriers below
+    float acc[4][MR];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int m = 0; m < MR; ++m) acc[r][m] = 0.f;
+    gemv_dot<T, MR>((const T*)p.X, p.ldx, (const T*)p.W, p.ldw, n0, p.M, p.K1, lane, acc);
+    if (p.K2 > 0) {
+        const int g = n0 / p.group;
+        if ((p.k2_mask >> g) & 1u)
+            gemv_dot<T, MR>((const T*)p.X2 + (int64_t)g * p.x2_group_stride, p.ldx2, (const T*)p.W2, p.ldw2, n0,
+                            p.M, p.K2, lane, acc);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int m = 0; m < MR; ++m) acc[r][m] = wave_sum(acc[r][m]);
+    if (lane == 0)
+#pragma unroll
+        for (int m = 0; m < MR; ++m)
+            if (m < p.M) epilogue4<T, EPI>(p, m, n0, f32x4{acc[0][m], acc[1][m], acc[2][m], acc[3][m]});
+}
+
+template <typename T, int EPI>
+hipError_t launch_gemv(const GemmParams& p, hipStream_t s) {
+    const dim3 grid((p.N / 4 + 3) / 4);
+#define PB_GEMV(MR) hipLaunchKernelGGL((gemv_kernel<T, EPI, MR>), grid, dim3(256), 0, s, p)
+    if (p.M <= 1) PB_GEMV(1);
+    else if (p.M <= 2) PB_GEMV(2);
+    else if (p.M <= 4) PB_GEMV(4);
+    else PB_GEMV(8);
+#undef PB_GEMV
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_gemv_typed(int role, const GemmParams& p, hipStream_t s) {
+    switch (role) {
+        case 0: return launch_gemv<T, EPI_QKV>(p, s);
+        case 1: case 3: return launch_gemv<T, EPI_RESID>(p, s);
+        case 2: return launch_gemv<T, EPI_RELU>(p, s);
+        case 4: return launch_gemv<T, EPI_SHRINK>(p, s);
+        default: break;
+    }
+    return hipErrorInvalidValue;
+}
+
 }  // namespace
 
 hipError_t launch_gemm(int dtype, int role, int epi, const GemmParams& p, const GemmWorkspace& wsp,
@@ -504,6 +600,8 @@ hipError_t launch_gemm(int dtype, int role, int epi, const GemmParams& p, const 
         return hipErrorInvalidValue;
     const int expect[5] = {EPI_QKV, EPI_RESID, EPI_RELU, EPI_RESID, EPI_SHRINK};
     if (role < 0 || role > 4 || expect[role] != epi) return hipErrorInvalidValue;
+    if (p.M <= GEMV_MAX_M && PB_GEMM_GEMV)
+        return dtype == 1 ? launch_gemv_typed<_Float16>(role, p, s) : launch_gemv_typed<__bf16>(role, p, s);
     if (dtype == 1) return launch_typed<_Float16>(role, p, wsp, s);
     return launch_typed<__bf16>(role, p, wsp, s);
 }

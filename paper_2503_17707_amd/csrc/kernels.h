@@ -102,6 +102,10 @@ hipError_t launch_argmax(const float* pval, const int* pidx, int B, int V, int32
 // the targets in mask) into slot `slot` of the packed per-layer arrays
 // Acat [L][4][kw][d] and Bcat [L][4][d][kw] (slot columns slot*rs .. +rs),
 // zero-filling ranks r..rs-1 and absent targets.
+// W [d, d] += scale * (slot's B [d, rs]) (slot's A [rs, d]), rounded once (misc.hip).
+hipError_t launch_lora_merge(int dtype, void* W, const void* Acat, const void* Bcat, int d, int kw, int rs,
+                             int slot, float scale, hipStream_t s);
+
 hipError_t launch_lora_pack(int dtype, const void* staging, size_t staging_layer_elems, int L,
                             int d, int r, uint32_t mask, int slot, int rs, int kw, void* Acat,
                             void* Bcat, hipStream_t s);

@@ -244,6 +244,40 @@ __global__ __launch_bounds__(256) void lora_pack_kernel(const T* __restrict__ st
     }
 }
 
+
+// ---- merged LoRA: W_t += s * B_t A_t in place ------------------------------
+// Thread (row n, columns 8c .. 8c+7) of target weight W [d, d]: the rank-rs
+// product of the slot's B rows (Bcat [d][kw], columns slot*rs ..) and A
+// columns (Acat [kw][d], rows slot*rs ..) in fp32, ranks in order, then one
+// rounding of W + s * product to dt.
+template <typename T>
+__global__ __launch_bounds__(256) void lora_merge_kernel(T* __restrict__ W, const T* __restrict__ Acat,
+                                                        const T* __restrict__ Bcat, int d, int kw,
+                                                        int rs, int slot, float scale) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int per_row = d / 8;
+    if (i >= (int64_t)d * per_row) return;
+    const int n = (int)(i / per_row), c = (int)(i % per_row) * 8;
+    float acc[8] = {};
+    const T* brow = Bcat + (int64_t)n * kw + (int64_t)slot * rs;
+    for (int j = 0; j < rs; ++j) {
+        const float b = (float)brow[j];
+        const u32x4 araw = *(const u32x4*)(Acat + ((int64_t)slot * rs + j) * d + c);
+        T a[8];
+        __builtin_memcpy(a, &araw, 16);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += b * (float)a[e];
+    }
+    T* w = W + (int64_t)n * d + c;
+    const u32x4 wraw = *(const u32x4*)w;
+    T wv[8];
+    __builtin_memcpy(wv, &wraw, 16);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) wv[e] = (T)((float)wv[e] + scale * acc[e]);
+    u32x4 out;
+    __builtin_memcpy(&out, wv, 16);
+    *(u32x4*)w = out;
+}
 }  // namespace
 
 hipError_t launch_embed(int dtype, const int32_t* tok, const void* E, const void* P, float* x,
@@ -357,6 +391,19 @@ hipError_t launch_lora_pack(int dtype, const void* staging, size_t staging_layer
         hipLaunchKernelGGL(lora_pack_kernel<__bf16>, grid, dim3(256), 0, s, (const __bf16*)staging,
                            staging_layer_elems, d, r, mask, slot, rs, kw, (__bf16*)Acat,
                            (__bf16*)Bcat);
+    return hipGetLastError();
+}
+
+hipError_t launch_lora_merge(int dtype, void* W, const void* Acat, const void* Bcat, int d, int kw, int rs,
+                             int slot, float scale, hipStream_t s) {
+    const int64_t threads = (int64_t)d * (d / 8);
+    const dim3 grid((unsigned)((threads + 255) / 256));
+    if (dtype == 1)
+        hipLaunchKernelGGL(lora_merge_kernel<_Float16>, grid, dim3(256), 0, s, (_Float16*)W, (const _Float16*)Acat,
+                           (const _Float16*)Bcat, d, kw, rs, slot, scale);
+    else
+        hipLaunchKernelGGL(lora_merge_kernel<__bf16>, grid, dim3(256), 0, s, (__bf16*)W, (const __bf16*)Acat,
+                           (const __bf16*)Bcat, d, kw, rs, slot, scale);
     return hipGetLastError();
 }
 

@@ -259,6 +259,7 @@ struct pb_model {
     hipEvent_t ring_ev[STAGE_SLOTS] = {};
     bool ring_busy[STAGE_SLOTS] = {};
     int ring_next = 0;
+    int merged_slot = -1;  // adapter merged into the device base weights (-1: none)
     // decode state: sequences of the last prefill, their length so far
     int dec_B = 0, dec_len = 0, dec_steps = 0;
     std::vector<int> dec_adapter;
@@ -587,6 +588,7 @@ int pb_stream_layers(pb_model* m, const int32_t* layer_order, int32_t n_layers,
     }
     HIP_TRY(hipEventRecord(m->ev_load0, m->copy));
     m->last_load_bytes = (double)gb + (double)L * (double)lb;
+    m->merged_slot = -1;  // the base weights arrive unmerged
     if (all_pinned) {
         // every copy is a DMA from locked pages: enqueue them all now
         const int rc = run_load(m, jobs);
@@ -649,6 +651,7 @@ int pb_poison_weights(pb_model* m, int32_t value) {
     for (int s = 0; s < MAX_SLOTS; ++s) m->slot_valid[s] = false;
     m->streamed = false;
     m->dec_B = 0;
+    m->merged_slot = -1;
     return PB_OK;
 }
 
@@ -907,6 +910,9 @@ static int run_forward(pb_model* m, const int32_t* tokens, int32_t B, int32_t T,
         const int a = adapter_of_seq ? adapter_of_seq[b] : -1;
         if (a < -1 || a >= c.max_adapters) return fail(PB_EINVAL, "adapter %d of sequence %d outside [-1, %d)", a, b, c.max_adapters);
         if (a >= 0) {
+            if (m->merged_slot >= 0)
+                return fail(PB_ESTATE, "adapter %d is merged into the base weights: sequences run with adapter -1",
+                            m->merged_slot);
             if (!m->slot_valid[a]) return fail(PB_ESTATE, "adapter slot %d holds no adapter", a);
             use_lora = true;
             lora_union |= m->slot_mask[a];
@@ -1007,6 +1013,35 @@ extern "C" int pb_rebuild_kv(pb_model* m, const int32_t* tokens, int32_t B, int3
     m->dec_steps = 0;
     m->dec_adapter.assign(B, -1);
     for (int b = 0; b < B; ++b) m->dec_adapter[b] = adapter_of_seq ? adapter_of_seq[b] : -1;
+    return PB_OK;
+}
+
+extern "C" int pb_merge_lora(pb_model* m, int32_t slot) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    const pb_config& c = m->cfg;
+    if (slot < 0 || slot >= c.max_adapters) return fail(PB_EINVAL, "slot %d outside [0, %d)", slot, c.max_adapters);
+    if (!m->slot_valid[slot]) return fail(PB_ESTATE, "adapter slot %d holds no adapter", slot);
+    if (!m->streamed) return fail(PB_ESTATE, "merge before pb_stream_layers");
+    if (m->merged_slot >= 0) return fail(PB_ESTATE, "adapter %d is already merged; stream the base layers again first", m->merged_slot);
+    const ArenaLayout& a = m->lay;
+    hipStream_t s = m->compute;
+    // every layer (and the adapter) must have landed before it is rewritten
+    if (m->lora_recorded) HIP_TRY(hipStreamWaitEvent(s, m->ev_lora, 0));
+    const int tensor_of[4] = {PB_T_WQ, PB_T_WK, PB_T_WV, PB_T_WO};
+    for (int l = 0; l < c.n_layers; ++l) {
+        if (int rc = wait_recorded(m, l)) return rc;
+        HIP_TRY(hipStreamWaitEvent(s, m->ev_layer[l], 0));
+        for (int t = 0; t < 4; ++t) {
+            if (!((m->slot_mask[slot] >> t) & 1u)) continue;
+            const char* At = m->at(a.loraA) + (size_t)l * a.loraA_layer + (size_t)t * a.kw * c.d_model * 2;
+            const char* Bt = m->at(a.loraB) + (size_t)l * a.loraB_layer + (size_t)t * c.d_model * a.kw * 2;
+            HIP_TRY(pb::launch_lora_merge(c.dtype, m->ltensor(l, tensor_of[t]), At, Bt, c.d_model, a.kw, a.rs, slot,
+                                          m->slot_scale[slot], s));
+        }
+    }
+    HIP_TRY(hipStreamSynchronize(s));
+    m->merged_slot = slot;
+    m->dec_B = 0;  // a KV cache from before the merge belongs to another model
     return PB_OK;
 }
 

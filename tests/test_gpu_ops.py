@@ -41,7 +41,10 @@ DT = {"bf16": 0, "f16": 1}
 
 @pytest.mark.parametrize("kind", ["f16", "bf16"])
 @pytest.mark.parametrize("M,N,K", [(37, 192, 128), (300, 384, 576), (512, 1024, 2048),
-                                   (1030, 768, 512), (1, 64, 64)])
+                                   (1030, 768, 512), (1, 64, 64),
+                                   # at most 8 rows: the weight-streaming path, K ragged
+                                   # against its 1024-column steps
+                                   (1, 2048, 2048), (3, 576, 1600), (8, 128, 8192)])
 @pytest.mark.parametrize("epi", [0, 1, 2])
 def test_gemm_epilogues(kind, M, N, K, epi):
     import torch
