@@ -189,6 +189,23 @@ int pb_prefill_first_token(pb_model* m, const int32_t* tokens, int32_t B, int32_
 int pb_decode_step(pb_model* m, const int32_t* tokens, int32_t B, const int32_t* adapter_of_seq,
                    int32_t* out_tokens, float* out_logits);
 
+/* Pipeline loading plan across GPUs (Sections 4.2.1 and 4.4.2), host only:
+ * the layer order each GPU of a server streams, after start-up or after some
+ * GPUs failed.  alive[g] != 0 for each of the n_gpus GPUs still running.  The
+ * alive GPUs, in index order, own consecutive blocks of layers (balance:
+ * sizes differ by at most one, the earlier blocks taking the remainder;
+ * contiguity: one run of layers each); GPU g's order lists its block first,
+ * then the layers after it, cyclically, so a pipeline over the alive GPUs can
+ * start once every block has landed while each GPU goes on to load the whole
+ * model.  order: int32 [n_gpus * n_layers], row g a permutation of
+ * 0..n_layers-1 for an alive GPU and all -1 for a failed one (pass a row to
+ * pb_stream_layers, skipping layers the GPU already holds); block_first,
+ * block_len: int32 [n_gpus] or NULL (-1 / 0 for failed GPUs).  With every GPU
+ * alive and n_gpus dividing n_layers, GPU g's order is the rotation starting
+ * at layer g * n_layers / n_gpus.  PB_EINVAL for bad sizes or no alive GPU. */
+int pb_plan_loading(int32_t n_layers, int32_t n_gpus, const uint8_t* alive, int32_t* order,
+                    int32_t* block_first, int32_t* block_len);
+
 /* Merged LoRA (Section 4.3.2): fold adapter slot `slot` into the device base
  * weights of every layer, W_t = dt(W_t + scale * B_t A_t) for each of its
  * targets (fp32 product, one rounding), on the compute stream after every

@@ -77,6 +77,9 @@ _SIGS = {
                                      ctypes.POINTER(ctypes.c_float)]),
     "pb_invalidate_kv": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_uint8), ctypes.c_int32]),
     "pb_merge_lora": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
+    "pb_plan_loading": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_uint8),
+                                       ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
+                                       ctypes.POINTER(ctypes.c_int32)]),
     "pb_decode_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
                                       ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
                                       ctypes.POINTER(ctypes.c_float)]),
@@ -450,6 +453,20 @@ def attach_all(m: Model, hw: HostWeights):
     for a in used:
         blobs = hw.loras.get(a) or hw.add_lora(a)
         m.attach_lora(a, blobs, w.lora_rank, w.lora_alpha, hw.lora_mask())
+
+
+def plan_loading(n_layers: int, alive: Sequence[bool]):
+    """Per-GPU layer orders and owned blocks (pb_plan_loading): returns
+    (orders [n_gpus][n_layers] with -1 rows for failed GPUs, [(first, len)] per GPU)."""
+    G = len(alive)
+    al = np.ascontiguousarray([1 if a else 0 for a in alive], dtype=np.uint8)
+    order = np.empty((G, n_layers), dtype=np.int32)
+    first = np.empty(G, dtype=np.int32)
+    ln = np.empty(G, dtype=np.int32)
+    p32 = ctypes.POINTER(ctypes.c_int32)
+    check(lib().pb_plan_loading(n_layers, G, al.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)),
+                                order.ctypes.data_as(p32), first.ctypes.data_as(p32), ln.ctypes.data_as(p32)))
+    return order, list(zip(first.tolist(), ln.tolist()))
 
 
 # ---- kernel-level entry points (include/pipeboost_ops.h) --------------------

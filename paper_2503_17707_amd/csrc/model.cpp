@@ -1016,6 +1016,35 @@ extern "C" int pb_rebuild_kv(pb_model* m, const int32_t* tokens, int32_t B, int3
     return PB_OK;
 }
 
+extern "C" int pb_plan_loading(int32_t n_layers, int32_t n_gpus, const uint8_t* alive, int32_t* order,
+                               int32_t* block_first, int32_t* block_len) {
+    if (n_layers < 1 || n_gpus < 1 || !alive || !order) return fail(PB_EINVAL, "bad arguments");
+    std::vector<int> live;
+    for (int g = 0; g < n_gpus; ++g)
+        if (alive[g]) live.push_back(g);
+    if (live.empty()) return fail(PB_EINVAL, "no GPU is alive");
+    const int n = (int)live.size();
+    for (int g = 0; g < n_gpus; ++g) {
+        for (int i = 0; i < n_layers; ++i) order[(size_t)g * n_layers + i] = -1;
+        if (block_first) block_first[g] = -1;
+        if (block_len) block_len[g] = 0;
+    }
+    // load balance: block sizes differ by at most one (earlier blocks take the
+    // remainder); layer contiguity: block k is one run of layers, in the
+    // order of the alive GPUs; each GPU loads its block, then the layers
+    // after it, cyclically
+    int first = 0;
+    for (int k = 0; k < n; ++k) {
+        const int len = n_layers / n + (k < n_layers % n ? 1 : 0);
+        const int g = live[k];
+        for (int i = 0; i < n_layers; ++i) order[(size_t)g * n_layers + i] = (first + i) % n_layers;
+        if (block_first) block_first[g] = first;
+        if (block_len) block_len[g] = len;
+        first += len;
+    }
+    return PB_OK;
+}
+
 extern "C" int pb_merge_lora(pb_model* m, int32_t slot) {
     if (!m) return fail(PB_EINVAL, "model is NULL");
     const pb_config& c = m->cfg;
