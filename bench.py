@@ -20,6 +20,7 @@ B=1, T=512, LoRA rank 16 on q and v, fp16 weights, random init) is synthetic.
 * cpu_baseline: the CPU oracle timed on a bounded sample of the same workload.
 """
 import argparse
+import gc
 import json
 import os
 import sys
@@ -260,6 +261,10 @@ def main():
     init_ms = (time.perf_counter() - t0) * 1e3
     toks = synth.tokens(w)
     ad = list(w.adapters())
+    # no collection passes of the interpreter inside timed regions (as timeit
+    # does): with torch loaded one pass stalls the host for tens of ms
+    gc.collect()
+    gc.disable()
 
     # ---- H2D alone (the bandwidth the loader can get): copies only, median of 3
     # after one warm-up transfer --------------------------------------------------
@@ -395,6 +400,7 @@ def main():
                   "max_abs_vs_unmerged": float(np.max(np.abs(ml - first[1])))}
     m.destroy()
     hw.free()
+    gc.enable()
 
     cpu = None
     if not args.no_cpu_baseline:

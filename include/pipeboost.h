@@ -249,6 +249,18 @@ int pb_set_chunk_bytes(pb_model* m, size_t bytes);
  * copy end) of the most recent pb_stream_layers; valid once it has completed. */
 int pb_last_load_stats(pb_model* m, double* bytes, double* ms);
 
+/* Graph replay of the forward pass (enabled by default).  Once every weight
+ * is resident (the last pb_stream_layers and pb_attach_lora have finished on
+ * the device), a forward shape (B, T, prefill or decode step, adapter targets
+ * in use) seen a second time is recorded as one HIP graph and replayed on
+ * later calls, so the host issues one launch instead of one per kernel.  The
+ * recorded kernels and their arguments are those of the launch-by-launch
+ * path, so results are bit-identical either way.  A load still in flight,
+ * kernel timing or a KV rebuild always runs launch by launch.  Up to 8 shapes
+ * are kept per model, least recently used evicted.  enable = 0 turns replay
+ * off (recorded graphs are kept for when it is turned on again). */
+int pb_set_graph_replay(pb_model* m, int32_t enable);
+
 /* Per-kernel timing of the forward pass.  When enabled, every kernel launch of
  * pb_prefill_first_token is bracketed by events on the compute stream and its
  * duration is added to a per-kernel-kind total (kinds PB_K_*). */

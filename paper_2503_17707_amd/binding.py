@@ -94,6 +94,7 @@ _SIGS = {
     "pb_last_load_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_double),
                                           ctypes.POINTER(ctypes.c_double)]),
     "pb_set_kernel_timing": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
+    "pb_set_graph_replay": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
     "pb_get_kernel_timing": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32,
                                             ctypes.POINTER(ctypes.c_double),
                                             ctypes.POINTER(ctypes.c_int64)]),
@@ -411,6 +412,10 @@ class Model:
         b, ms = ctypes.c_double(), ctypes.c_double()
         check(lib().pb_last_load_stats(self.h, ctypes.byref(b), ctypes.byref(ms)))
         return b.value, ms.value
+
+    def set_graph_replay(self, on: bool):
+        """Record settled forward shapes as HIP graphs and replay them (default on)."""
+        check(lib().pb_set_graph_replay(self.h, 1 if on else 0))
 
     def set_timing(self, on: bool):
         check(lib().pb_set_kernel_timing(self.h, 1 if on else 0))

@@ -297,7 +297,8 @@ constexpr int DEC_KEYS = 256;
 template <typename T, int HD>
 __global__ __launch_bounds__(256) void decode_attention_kernel(const T* __restrict__ qkv,
                                                               const T* __restrict__ kv,
-                                                              int64_t seq_stride, int d, int nkeys,
+                                                              int64_t seq_stride, int d,
+                                                              const int32_t* __restrict__ pos0,
                                                               float* __restrict__ part, int nsplit) {
     constexpr int DPL = HD / 64;  // head dimensions per lane in the P V product
     __shared__ float qs[HD];
@@ -306,6 +307,8 @@ __global__ __launch_bounds__(256) void decode_attention_kernel(const T* __restri
     __shared__ float wo[4][HD];
     const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     const int H = gridDim.y;
+    const int nkeys = *pos0 + 1;
+    if (split * DEC_KEYS >= nkeys) return;  // past the live keys: the combine reads only live splits
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const T* q = qkv + (int64_t)b * 3 * d + h * HD;
     for (int i = threadIdx.x; i < HD; i += 256) qs[i] = (float)q[i];
@@ -369,14 +372,16 @@ __global__ __launch_bounds__(256) void decode_attention_kernel(const T* __restri
 
 template <typename T, int HD>
 __global__ __launch_bounds__(HD) void decode_combine_kernel(const float* __restrict__ part, int nsplit,
-                                                           int d, T* __restrict__ out) {
+                                                           const int32_t* __restrict__ pos0, int d,
+                                                           T* __restrict__ out) {
     const int h = blockIdx.x, b = blockIdx.y, H = gridDim.x;
     const int dim = threadIdx.x;
+    const int live = (*pos0 + DEC_KEYS) / DEC_KEYS;  // splits holding keys 0 .. *pos0
     const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
     float M = -INFINITY;
-    for (int sp = 0; sp < nsplit; ++sp) M = fmaxf(M, pp[sp * (HD + 2)]);
+    for (int sp = 0; sp < live; ++sp) M = fmaxf(M, pp[sp * (HD + 2)]);
     float acc = 0.f, L = 0.f;
-    for (int sp = 0; sp < nsplit; ++sp) {
+    for (int sp = 0; sp < live; ++sp) {
         const float ms = pp[sp * (HD + 2)];
         if (ms == -INFINITY) continue;
         const float f = __builtin_amdgcn_exp2f((ms - M) * LOG2E);
@@ -387,15 +392,16 @@ __global__ __launch_bounds__(HD) void decode_combine_kernel(const float* __restr
 }
 
 template <typename T, int HD>
-hipError_t launch_decode_hd(const void* qkv, const void* kv, int64_t seq_stride, int B, int H, int nkeys,
-                            float* part, void* out, hipStream_t s) {
+hipError_t launch_decode_hd(const void* qkv, const void* kv, int64_t seq_stride, int B, int H,
+                            const int32_t* pos0, int max_keys, float* part, void* out, hipStream_t s) {
     const int d = H * HD;
-    const int nsplit = (nkeys + DEC_KEYS - 1) / DEC_KEYS;
+    const int nsplit = (max_keys + DEC_KEYS - 1) / DEC_KEYS;
     hipLaunchKernelGGL((decode_attention_kernel<T, HD>), dim3(nsplit, H, B), dim3(256), 0, s, (const T*)qkv,
-                       (const T*)kv, seq_stride, d, nkeys, part, nsplit);
+                       (const T*)kv, seq_stride, d, pos0, part, nsplit);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((decode_combine_kernel<T, HD>), dim3(H, B), dim3(HD), 0, s, part, nsplit, d, (T*)out);
+    hipLaunchKernelGGL((decode_combine_kernel<T, HD>), dim3(H, B), dim3(HD), 0, s, part, nsplit, pos0, d,
+                       (T*)out);
     return hipGetLastError();
 }
 }  // namespace
@@ -428,16 +434,16 @@ size_t decode_attention_part_floats(int B, int H, int hd, int max_keys) {
 }
 
 hipError_t launch_decode_attention(int dtype, const void* qkv, const void* kv, int64_t seq_stride,
-                                   int B, int H, int hd, int nkeys, float* part, void* out,
-                                   hipStream_t s) {
+                                   int B, int H, int hd, const int32_t* pos0, int max_keys, float* part,
+                                   void* out, hipStream_t s) {
     if (B <= 0) return hipSuccess;
-    if (nkeys <= 0) return hipErrorInvalidValue;
+    if (max_keys <= 0 || !pos0) return hipErrorInvalidValue;
     if (dtype == 1) {
-        if (hd == 64) return launch_decode_hd<_Float16, 64>(qkv, kv, seq_stride, B, H, nkeys, part, out, s);
-        if (hd == 128) return launch_decode_hd<_Float16, 128>(qkv, kv, seq_stride, B, H, nkeys, part, out, s);
+        if (hd == 64) return launch_decode_hd<_Float16, 64>(qkv, kv, seq_stride, B, H, pos0, max_keys, part, out, s);
+        if (hd == 128) return launch_decode_hd<_Float16, 128>(qkv, kv, seq_stride, B, H, pos0, max_keys, part, out, s);
     } else {
-        if (hd == 64) return launch_decode_hd<__bf16, 64>(qkv, kv, seq_stride, B, H, nkeys, part, out, s);
-        if (hd == 128) return launch_decode_hd<__bf16, 128>(qkv, kv, seq_stride, B, H, nkeys, part, out, s);
+        if (hd == 64) return launch_decode_hd<__bf16, 64>(qkv, kv, seq_stride, B, H, pos0, max_keys, part, out, s);
+        if (hd == 128) return launch_decode_hd<__bf16, 128>(qkv, kv, seq_stride, B, H, pos0, max_keys, part, out, s);
     }
     return hipErrorInvalidValue;
 }

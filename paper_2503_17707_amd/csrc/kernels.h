@@ -64,21 +64,27 @@ hipError_t launch_attention(int dtype, const void* qkv, void* out, int B, int T,
 hipError_t launch_attention_kv(int dtype, const void* qkv, const void* kv, int64_t kv_ld, int64_t kv_seq,
                                void* out, int B, int T, int H, int hd, hipStream_t s);
 
-// x[b*T + t, :] = E[tok[b*T + t], :] + P[t, :] (fp32 output).
+// x[b*T + t, :] = E[tok[b*T + t], :] + P[pos0 + t, :] (fp32 output), with
+// pos0 read from device memory (*pos0) so that replays of a recorded launch
+// can move it.
 hipError_t launch_embed(int dtype, const int32_t* tok, const void* E, const void* P, float* x,
-                        int n_rows, int T, int d, hipStream_t s, int pos0 = 0);
+                        int n_rows, int T, int d, const int32_t* pos0, hipStream_t s);
 
-// Keys and values of n_rows token rows of qkv into the KV cache (see misc.hip).
-hipError_t launch_kv_store(int dtype, const void* qkv, int n_rows, int T_len, int pos0, int d,
+// Keys and values of n_rows token rows of qkv into the KV cache at positions
+// *pos0 + t (see misc.hip).
+hipError_t launch_kv_store(int dtype, const void* qkv, int n_rows, int T_len, const int32_t* pos0, int d,
                            void* kv, int64_t seq_stride, hipStream_t s);
 
 // One new query per (sequence, head) of qkv ([B, 3d], q pre-scaled) against
-// cache positions 0 .. nkeys-1 of kv ([B][seq_stride], rows [k | v] of 2d);
-// out [B, d].  part: scratch of decode_attention_part_floats(B, H, hd, nkeys).
+// cache positions 0 .. *pos0 of kv ([B][seq_stride], rows [k | v] of 2d), the
+// last one the new token's own; out [B, d].  The grid covers max_keys keys
+// whatever *pos0 holds (blocks past the live keys leave at once), so one
+// launch serves every step.  part: scratch of
+// decode_attention_part_floats(B, H, hd, max_keys).
 size_t decode_attention_part_floats(int B, int H, int hd, int max_keys);
 hipError_t launch_decode_attention(int dtype, const void* qkv, const void* kv, int64_t seq_stride,
-                                   int B, int H, int hd, int nkeys, float* part, void* out,
-                                   hipStream_t s);
+                                   int B, int H, int hd, const int32_t* pos0, int max_keys, float* part,
+                                   void* out, hipStream_t s);
 
 // out[r, :] = LN(x[r * in_mul + in_add, :]) * g + b, fp32 statistics;
 // out_f32 selects a float output, otherwise dt.

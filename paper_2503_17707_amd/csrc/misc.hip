@@ -15,9 +15,9 @@ __global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ 
                                                    const T* __restrict__ E,
                                                    const T* __restrict__ P,
                                                    float* __restrict__ x, int T_len, int d,
-                                                   int pos0) {
+                                                   const int32_t* __restrict__ pos0) {
     const int row = blockIdx.x;
-    const int t = pos0 + row % T_len;
+    const int t = *pos0 + row % T_len;
     const T* e = E + (int64_t)tok[row] * d;
     const T* pp = P + (int64_t)t * d;
     float* xr = x + (int64_t)row * d;
@@ -281,7 +281,7 @@ __global__ __launch_bounds__(256) void lora_merge_kernel(T* __restrict__ W, cons
 }  // namespace
 
 hipError_t launch_embed(int dtype, const int32_t* tok, const void* E, const void* P, float* x,
-                        int n_rows, int T_len, int d, hipStream_t s, int pos0) {
+                        int n_rows, int T_len, int d, const int32_t* pos0, hipStream_t s) {
     if (n_rows <= 0) return hipSuccess;
     if (dtype == 1)
         hipLaunchKernelGGL(embed_kernel<_Float16>, dim3(n_rows), dim3(256), 0, s, tok,
@@ -295,17 +295,18 @@ hipError_t launch_embed(int dtype, const int32_t* tok, const void* E, const void
 // ---- KV cache: keys and values of token rows into their cache positions ----
 // Row r of qkv ([N, 3d], sequence-major, T_len rows per sequence) holds the
 // key at columns [d, 2d) and the value at [2d, 3d); they go to cache row
-// (sequence r / T_len, position pos0 + r % T_len) of kv ([B][seq_rows][2d]).
+// (sequence r / T_len, position *pos0 + r % T_len) of kv ([B][seq_rows][2d]).
 template <typename T>
 __global__ __launch_bounds__(256) void kv_store_kernel(const T* __restrict__ qkv, int d, int T_len,
-                                                      int pos0, T* __restrict__ kv, int64_t seq_stride) {
+                                                      const int32_t* __restrict__ pos0, T* __restrict__ kv,
+                                                      int64_t seq_stride) {
     const int r = blockIdx.x;
     const T* src = qkv + (int64_t)r * 3 * d + d;
-    T* dst = kv + (int64_t)(r / T_len) * seq_stride + (int64_t)(pos0 + r % T_len) * 2 * d;
+    T* dst = kv + (int64_t)(r / T_len) * seq_stride + (int64_t)(*pos0 + r % T_len) * 2 * d;
     for (int c = threadIdx.x * 8; c < 2 * d; c += 256 * 8) *(u32x4*)(dst + c) = *(const u32x4*)(src + c);
 }
 
-hipError_t launch_kv_store(int dtype, const void* qkv, int n_rows, int T_len, int pos0, int d,
+hipError_t launch_kv_store(int dtype, const void* qkv, int n_rows, int T_len, const int32_t* pos0, int d,
                            void* kv, int64_t seq_stride, hipStream_t s) {
     if (n_rows <= 0) return hipSuccess;
     if (dtype == 1)

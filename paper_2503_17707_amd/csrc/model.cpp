@@ -9,7 +9,10 @@
 // layer l starts the moment its bytes have landed, while later layers are
 // still crossing PCIe.  The compute schedule (kernel sequence, tiling,
 // reduction orders) never depends on the load order, so results are
-// bit-identical for any order.
+// bit-identical for any order.  Once the weights are resident, a repeated forward
+// shape is recorded as one HIP graph and replayed (the same launches, no
+// per-kernel host work), which matters for warm prefills and decode steps
+// whose kernels are short.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -51,6 +54,11 @@ int fail(int code, const char* fmt, ...) {
 
 constexpr size_t ALIGN = 256;
 constexpr int MAX_SLOTS = 16;
+// per-call scalars uploaded in one copy: MAX_SLOTS adapter scales, then the
+// position of the first new token
+constexpr int SMALL_WORDS = MAX_SLOTS + 1;
+// recorded forward passes kept per model (least recently used evicted)
+constexpr size_t MAX_GRAPHS = 8;
 constexpr int MAX_RANK = 64;
 constexpr size_t VEC_ALIGN = 128;  // elements (256 bytes of dt)
 // split-K partials: room for 4 fp32 partials of a [max_tokens, d_model]
@@ -194,7 +202,7 @@ ArenaLayout arena_layout(const pb_config* c) {
     a.z = take(N * 4 * (size_t)a.kw * 2);
     a.rowslot = take(N * 4);
     a.tokens = take(N * 4);
-    a.slotscale = take(MAX_SLOTS * 4);
+    a.slotscale = take(SMALL_WORDS * 4);
     a.zf = take(B * d * 4);
     a.logits = take(B * V * 4);
     a.outtok = take(B * 4);
@@ -276,6 +284,18 @@ struct pb_model {
     float* h_scale = nullptr;
     int32_t* h_outtok = nullptr;
     float* h_logits = nullptr;
+    // recorded forward passes, replayed once the weights have settled; an
+    // entry with no exec has been seen once (a shape seen once is not recorded)
+    struct Graph {
+        int B, T;
+        bool decode, use_lora;
+        uint32_t lora_union;
+        hipGraphExec_t exec;
+        uint64_t last_use;
+    };
+    std::vector<Graph> graphs;
+    uint64_t graph_clock = 0;
+    bool graphs_on = true;
     // per-kernel timing
     bool timing = false;
     std::vector<hipEvent_t> tev;
@@ -406,7 +426,7 @@ int pb_model_create(const pb_config* cfg, void* dev_arena, size_t arena_bytes, v
     const size_t B = cfg->max_batch, N = cfg->max_tokens, V = cfg->vocab;
     if (hipHostMalloc((void**)&m->h_tokens, N * 4, 0) != hipSuccess ||
         hipHostMalloc((void**)&m->h_rowslot, N * 4, 0) != hipSuccess ||
-        hipHostMalloc((void**)&m->h_scale, MAX_SLOTS * 4, 0) != hipSuccess ||
+        hipHostMalloc((void**)&m->h_scale, SMALL_WORDS * 4, 0) != hipSuccess ||
         hipHostMalloc((void**)&m->h_outtok, B * 4, 0) != hipSuccess ||
         hipHostMalloc((void**)&m->h_logits, B * V * 4, 0) != hipSuccess)
         return cleanup(fail(PB_ENOMEM, "pinned staging allocation failed"));
@@ -433,6 +453,8 @@ int pb_destroy(pb_model* m) {
         if (e) (void)hipEventDestroy(e);
     for (auto e : {m->ev_globals, m->ev_lora, m->ev_load0, m->ev_load1})
         if (e) (void)hipEventDestroy(e);
+    for (auto& g : m->graphs)
+        if (g.exec) (void)hipGraphExecDestroy(g.exec);
     for (void* p : {(void*)m->h_tokens, (void*)m->h_rowslot, (void*)m->h_scale, (void*)m->h_outtok,
                     (void*)m->h_logits})
         if (p) (void)hipHostFree(p);
@@ -667,6 +689,12 @@ int pb_last_load_stats(pb_model* m, double* bytes, double* ms) {
     return PB_OK;
 }
 
+int pb_set_graph_replay(pb_model* m, int32_t enable) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    m->graphs_on = enable != 0;
+    return PB_OK;
+}
+
 int pb_set_kernel_timing(pb_model* m, int32_t enable) {
     if (!m) return fail(PB_EINVAL, "model is NULL");
     m->timing = enable != 0;
@@ -719,11 +747,14 @@ struct Timed {
 };
 
 // The forward pass of B sequences of T new tokens at positions pos0 ..
-// pos0+T-1.  A prefill (decode = false) attends among its own tokens; a decode
-// step (T = 1) attends to the KV cache, which both append to when the model
-// keeps one.
-int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_union, int pos0 = 0,
-                    bool decode = false, const uint8_t* has_kv = nullptr) {
+// pos0+T-1, pos0 read from device memory.  A prefill (decode = false) attends
+// among its own tokens; a decode step (T = 1) attends to the KV cache, which
+// both append to when the model keeps one.  With wait_loads the compute
+// stream waits for each layer's copy event before the layer's first kernel
+// (the pipelined cold start); without, every weight must already be resident
+// (a recorded pass holds no waits on the load's events).
+int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_union, bool decode,
+                    const uint8_t* has_kv, bool wait_loads) {
     const pb_config& c = m->cfg;
     const ArenaLayout& a = m->lay;
     const int dt = c.dtype;
@@ -740,14 +771,20 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
     const int32_t* rowslot = (const int32_t*)m->at(a.rowslot);
     const float* sscale = (const float*)m->at(a.slotscale);
     const pb::GemmWorkspace gws{m->at(a.ws), a.ws_bytes};
+    const int32_t* pos0 = (const int32_t*)(m->at(a.slotscale) + MAX_SLOTS * 4);
+    auto wait_layer = [&](int l) -> int {
+        if (!wait_loads) return PB_OK;
+        if (int rc = wait_recorded(m, l)) return rc;
+        HIP_TRY(hipStreamWaitEvent(s, l < 0 ? m->ev_globals : m->ev_layer[l], 0));
+        return PB_OK;
+    };
 
-    if (int rc = wait_recorded(m, -1)) return rc;
-    HIP_TRY(hipStreamWaitEvent(s, m->ev_globals, 0));
-    if (use_lora) HIP_TRY(hipStreamWaitEvent(s, m->ev_lora, 0));
+    if (int rc = wait_layer(-1)) return rc;
+    if (use_lora && wait_loads) HIP_TRY(hipStreamWaitEvent(s, m->ev_lora, 0));
     {
         Timed t(m, PB_K_EMBED);
         HIP_TRY(pb::launch_embed(dt, (const int32_t*)m->at(a.tokens), m->gtensor(PB_G_EMBED),
-                                 m->gtensor(PB_G_POS), x, N, T, d, s, pos0));
+                                 m->gtensor(PB_G_POS), x, N, T, d, pos0, s));
     }
     const bool qkv_lora = use_lora && (lora_union & (PB_LORA_Q | PB_LORA_K | PB_LORA_V));
     const bool o_lora = use_lora && (lora_union & PB_LORA_O);
@@ -765,8 +802,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
     };
     bool ln1_ready = false;  // LN1 (and its fused shrink) of layer l produced by layer l-1's fc2 reduce
     for (int l = 0; l < L; ++l) {
-        if (int rc = wait_recorded(m, l)) return rc;
-        HIP_TRY(hipStreamWaitEvent(s, m->ev_layer[l], 0));
+        if (int rc = wait_layer(l)) return rc;
         char* Aq = m->at(a.loraA) + (size_t)l * a.loraA_layer;  // [4][kw][d]
         char* Bq = m->at(a.loraB) + (size_t)l * a.loraB_layer;  // [4][d][kw]
         if (!ln1_ready) {
@@ -815,7 +851,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
                 HIP_TRY(pb::launch_attention(dt, qkv, attn, B, T, H, hd, s));
             } else {
                 const char* kvl = m->at(a.kv) + (size_t)l * a.kv_layer * 2;
-                HIP_TRY(pb::launch_decode_attention(dt, qkv, kvl, (int64_t)a.kv_seq, B, H, hd, pos0 + 1,
+                HIP_TRY(pb::launch_decode_attention(dt, qkv, kvl, (int64_t)a.kv_seq, B, H, hd, pos0, c.max_pos,
                                                     (float*)m->at(a.dec_part), attn, s));
             }
         }
@@ -865,8 +901,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             // the next layer's LN1 rides on the split-K reduce when the launcher
             // splits; its weights are read here, so wait for that layer first
             if (l + 1 < L) {
-                if (int rc = wait_recorded(m, l + 1)) return rc;
-                HIP_TRY(hipStreamWaitEvent(s, m->ev_layer[l + 1], 0));
+                if (int rc = wait_layer(l + 1)) return rc;
                 p.ln_g = m->ltensor(l + 1, PB_T_LN1_G); p.ln_b = m->ltensor(l + 1, PB_T_LN1_B);
                 p.ln_out = u; p.ln_eps = c.ln_eps; p.ln_done = &ln1_ready;
                 p.shrink = row_shrink_args(l + 1);
@@ -890,6 +925,64 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
         HIP_TRY(pb::launch_argmax((const float*)m->at(a.pval), (const int*)m->at(a.pidx), B, c.vocab,
                                   (int32_t*)m->at(a.outtok), s));
     }
+    return PB_OK;
+}
+
+// True once every weight the forward pass reads is resident: the last load
+// (and adapter attach, when adapters are used) has finished on the device.
+bool weights_settled(pb_model* m, bool use_lora) {
+    if (!m->streamed) return false;
+    {
+        std::lock_guard<std::mutex> lk(m->mu);
+        if (!m->load_done || m->load_rc || !m->globals_ready) return false;
+        for (char r : m->ready)
+            if (!r) return false;
+    }
+    if (hipEventQuery(m->ev_load1) != hipSuccess) return false;
+    if (use_lora && (!m->lora_recorded || hipEventQuery(m->ev_lora) != hipSuccess)) return false;
+    return true;
+}
+
+// The forward pass as one graph launch: the launches of a shape are recorded
+// the second time the shape is seen (every kernel argument is a function of
+// the shape, the adapter targets in use and the fixed arena; the inputs,
+// including the position, live in device memory) and replayed from then on.
+// Returns 1 when the caller should launch eagerly instead (first sight).
+int forward_graph(pb_model* m, int B, int T, bool use_lora, uint32_t lora_union, bool decode) {
+    pb_model::Graph* g = nullptr;
+    for (auto& e : m->graphs)
+        if (e.B == B && e.T == T && e.decode == decode && e.use_lora == use_lora && e.lora_union == lora_union)
+            g = &e;
+    if (!g) {
+        if (m->graphs.size() >= MAX_GRAPHS) {
+            auto old = std::min_element(m->graphs.begin(), m->graphs.end(),
+                                        [](const pb_model::Graph& a, const pb_model::Graph& b) {
+                                            return a.last_use < b.last_use;
+                                        });
+            if (old->exec) (void)hipGraphExecDestroy(old->exec);
+            m->graphs.erase(old);
+        }
+        m->graphs.push_back({B, T, decode, use_lora, lora_union, nullptr, ++m->graph_clock});
+        return 1;
+    }
+    g->last_use = ++m->graph_clock;
+    hipStream_t s = m->compute;
+    if (!g->exec) {
+        hipGraph_t graph = nullptr;
+        HIP_TRY(hipStreamBeginCapture(s, hipStreamCaptureModeRelaxed));
+        const int rc = enqueue_forward(m, B, T, use_lora, lora_union, decode, nullptr, false);
+        const hipError_t e = hipStreamEndCapture(s, &graph);
+        if (rc || e != hipSuccess) {
+            if (graph) (void)hipGraphDestroy(graph);
+            return rc ? rc : fail(PB_EHIP, "recording the forward pass failed: %s", hipGetErrorString(e));
+        }
+        hipGraphExec_t exec = nullptr;
+        const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+        (void)hipGraphDestroy(graph);
+        if (ei != hipSuccess) return fail(PB_EHIP, "hipGraphInstantiate failed: %s", hipGetErrorString(ei));
+        g->exec = exec;
+    }
+    HIP_TRY(hipGraphLaunch(g->exec, s));
     return PB_OK;
 }
 
@@ -921,13 +1014,17 @@ static int run_forward(pb_model* m, const int32_t* tokens, int32_t B, int32_t T,
     }
     std::memcpy(m->h_tokens, tokens, (size_t)N * 4);
     for (int s = 0; s < MAX_SLOTS; ++s) m->h_scale[s] = m->slot_valid[s] ? m->slot_scale[s] : 0.f;
+    std::memcpy(&m->h_scale[MAX_SLOTS], &pos0, 4);
     const ArenaLayout& a = m->lay;
     hipStream_t s = m->compute;
     m->tused = 0;
     HIP_TRY(hipMemcpyAsync(m->at(a.tokens), m->h_tokens, (size_t)N * 4, hipMemcpyHostToDevice, s));
     HIP_TRY(hipMemcpyAsync(m->at(a.rowslot), m->h_rowslot, (size_t)N * 4, hipMemcpyHostToDevice, s));
-    HIP_TRY(hipMemcpyAsync(m->at(a.slotscale), m->h_scale, MAX_SLOTS * 4, hipMemcpyHostToDevice, s));
-    int rc = enqueue_forward(m, B, T, use_lora, lora_union, pos0, decode, has_kv);
+    HIP_TRY(hipMemcpyAsync(m->at(a.slotscale), m->h_scale, SMALL_WORDS * 4, hipMemcpyHostToDevice, s));
+    int rc = 1;
+    if (m->graphs_on && !m->timing && !has_kv && weights_settled(m, use_lora))
+        rc = forward_graph(m, B, T, use_lora, lora_union, decode);
+    if (rc == 1) rc = enqueue_forward(m, B, T, use_lora, lora_union, decode, has_kv, true);
     if (rc) {
         (void)hipStreamSynchronize(s);
         return rc;
