@@ -287,121 +287,121 @@ hipError_t launch_qw(const void* qkv, const void* kv, int64_t kv_ld, int64_t kv_
 }
 
 // ---- decode: one new query per (sequence, head) against the KV cache --------
-// Split over keys (256 per block, 64 per wave): each lane scores one key
-// (fp32 dot product with the query, held in LDS), each wave takes its own max
-// and sum, then lanes switch to head dimensions to accumulate P V over the
-// wave's keys.  Blocks write (max, sum, o) partials; a second kernel combines
-// the splits of each (sequence, head) in split order.
-constexpr int DEC_KEYS = 256;
-
-template <typename T, int HD>
-__global__ __launch_bounds__(256) void decode_attention_kernel(const T* __restrict__ qkv,
-                                                              const T* __restrict__ kv,
-                                                              int64_t seq_stride, int d,
-                                                              const int32_t* __restrict__ pos0,
-                                                              float* __restrict__ part, int nsplit) {
-    constexpr int DPL = HD / 64;  // head dimensions per lane in the P V product
-    __shared__ float qs[HD];
-    __shared__ float ps[4][64];
-    __shared__ float wm[4], wl[4];
-    __shared__ float wo[4][HD];
-    const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-    const int H = gridDim.y;
+// One block per (sequence, head); its NW waves take 64-key chunks in turn
+// (wave w: keys 64w.., then 64(w + NW).., ...) with a running max and sum.  A
+// key row of HD elements is read by G = HD / 8 lanes, 16 bytes each, so one
+// load instruction covers 64 / G whole keys, and a wave issues all the K and
+// V loads of a chunk before using any.  Scores are fp32 dot products with the
+// query (reduced over the G lanes of a key); P V accumulates 8 head
+// dimensions per lane, reduced at the end over the lanes that hold the same
+// dimensions; the waves are combined through LDS in wave order.
+template <typename T, int HD, int NW>
+__global__ __launch_bounds__(64 * NW) void decode_attention_kernel(const T* __restrict__ qkv,
+                                                                   const T* __restrict__ kv, int64_t seq_stride,
+                                                                   int d, const int32_t* __restrict__ pos0,
+                                                                   T* __restrict__ out) {
+    constexpr int G = HD / 8;     // lanes per key row
+    constexpr int KPI = 64 / G;   // keys per load instruction
+    constexpr int NI = 64 / KPI;  // load instructions per 64-key chunk
+    __shared__ float wm[NW], wl[NW];
+    __shared__ float wo[NW][HD];
+    const int h = blockIdx.x, b = blockIdx.y;
     const int nkeys = *pos0 + 1;
-    if (split * DEC_KEYS >= nkeys) return;  // past the live keys: the combine reads only live splits
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const T* q = qkv + (int64_t)b * 3 * d + h * HD;
-    for (int i = threadIdx.x; i < HD; i += 256) qs[i] = (float)q[i];
-    __syncthreads();
-    const T* kvb = kv + (int64_t)b * seq_stride;
-    const int kbase = split * DEC_KEYS + wave * 64;
-    const int key = kbase + lane;
-    const bool valid = key < nkeys;
-    const T* krow = kvb + (int64_t)min(key, nkeys - 1) * 2 * d + h * HD;
-    float sc = 0.f;
-#pragma unroll
-    for (int c = 0; c < HD; c += 8) {
-        const u32x4 raw = *(const u32x4*)(krow + c);
+    const int sub = lane % G, grp = lane / G;
+    float q[8];
+    {
+        const u32x4 raw = *(const u32x4*)(qkv + (int64_t)b * 3 * d + h * HD + sub * 8);
         T e[8];
         __builtin_memcpy(e, &raw, 16);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) sc += (float)e[j] * qs[c + j];
+        for (int j = 0; j < 8; ++j) q[j] = (float)e[j];
     }
-    sc = valid ? sc : -INFINITY;
-    const float m = wave_max(sc);  // -inf only for a wave with no key
-    const float pk = valid ? __builtin_amdgcn_exp2f((sc - m) * LOG2E) : 0.f;
-    const float l = wave_sum(pk);
-    ps[wave][lane] = pk;
-    __syncthreads();
-    float o[DPL];
+    const T* kvb = kv + (int64_t)b * seq_stride + h * HD + sub * 8;
+    float m_run = -INFINITY, l = 0.f, o[8];
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) o[e] = 0.f;
-    const int nk = max(0, min(64, nkeys - kbase));
-    for (int j = 0; j < nk; ++j) {
-        const T* vrow = kvb + (int64_t)(kbase + j) * 2 * d + d + h * HD + lane * DPL;
-        const float p = ps[wave][j];
+    for (int j = 0; j < 8; ++j) o[j] = 0.f;
+    for (int c0 = wave * 64; c0 < nkeys; c0 += NW * 64) {  // wave-uniform
+        u32x4 kr[NI], vr[NI];
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) o[e] += p * (float)vrow[e];
+        for (int i = 0; i < NI; ++i) {
+            const int key = min(c0 + i * KPI + grp, nkeys - 1);
+            kr[i] = *(const u32x4*)(kvb + (int64_t)key * 2 * d);
+        }
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int key = min(c0 + i * KPI + grp, nkeys - 1);
+            vr[i] = *(const u32x4*)(kvb + (int64_t)key * 2 * d + d);
+        }
+        float sc[NI];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            T e[8];
+            __builtin_memcpy(e, &kr[i], 16);
+            float a = 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) a += q[j] * (float)e[j];
+#pragma unroll
+            for (int sh = 1; sh < G; sh <<= 1) a += __shfl_xor(a, sh, 64);
+            sc[i] = c0 + i * KPI + grp < nkeys ? a : -INFINITY;
+            mx = fmaxf(mx, sc[i]);
+        }
+        const float m_new = fmaxf(m_run, wave_max(mx));  // finite: the chunk holds a live key
+        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * LOG2E);
+        l *= alpha;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) o[j] *= alpha;
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const float pk = sc[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((sc[i] - m_new) * LOG2E);
+            l += pk;
+            T e[8];
+            __builtin_memcpy(e, &vr[i], 16);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) o[j] += pk * (float)e[j];
+        }
+        m_run = m_new;
+    }
+    // over the lanes holding the same dimensions (the KPI key groups)
+#pragma unroll
+    for (int sh = G; sh < 64; sh <<= 1) {
+        l += __shfl_xor(l, sh, 64);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) o[j] += __shfl_xor(o[j], sh, 64);
     }
     if (lane == 0) {
-        wm[wave] = m;
+        wm[wave] = m_run;
         wl[wave] = l;
     }
+    if (grp == 0)
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) wo[wave][lane * DPL + e] = o[e];
+        for (int j = 0; j < 8; ++j) wo[wave][sub * 8 + j] = o[j];
     __syncthreads();
-    if (threadIdx.x < HD) {
-        const int dim = threadIdx.x;
-        const float M = fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3]));
+    const int dim = threadIdx.x;
+    if (dim < HD) {
+        float M = wm[0];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) M = fmaxf(M, wm[w]);
         float acc = 0.f, L = 0.f;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-            if (wm[w] == -INFINITY) continue;
+        for (int w = 0; w < NW; ++w) {
+            if (wm[w] == -INFINITY) continue;  // a wave with no key
             const float f = __builtin_amdgcn_exp2f((wm[w] - M) * LOG2E);
             acc += f * wo[w][dim];
             L += f * wl[w];
         }
-        float* out = part + (((int64_t)b * H + h) * nsplit + split) * (HD + 2);
-        out[2 + dim] = acc;
-        if (dim == 0) {
-            out[0] = M;
-            out[1] = L;
-        }
+        out[(int64_t)b * d + h * HD + dim] = (T)(acc / L);
     }
-}
-
-template <typename T, int HD>
-__global__ __launch_bounds__(HD) void decode_combine_kernel(const float* __restrict__ part, int nsplit,
-                                                           const int32_t* __restrict__ pos0, int d,
-                                                           T* __restrict__ out) {
-    const int h = blockIdx.x, b = blockIdx.y, H = gridDim.x;
-    const int dim = threadIdx.x;
-    const int live = (*pos0 + DEC_KEYS) / DEC_KEYS;  // splits holding keys 0 .. *pos0
-    const float* pp = part + ((int64_t)b * H + h) * nsplit * (HD + 2);
-    float M = -INFINITY;
-    for (int sp = 0; sp < live; ++sp) M = fmaxf(M, pp[sp * (HD + 2)]);
-    float acc = 0.f, L = 0.f;
-    for (int sp = 0; sp < live; ++sp) {
-        const float ms = pp[sp * (HD + 2)];
-        if (ms == -INFINITY) continue;
-        const float f = __builtin_amdgcn_exp2f((ms - M) * LOG2E);
-        acc += f * pp[sp * (HD + 2) + 2 + dim];
-        L += f * pp[sp * (HD + 2) + 1];
-    }
-    out[(int64_t)b * d + h * HD + dim] = (T)(acc / L);
 }
 
 template <typename T, int HD>
 hipError_t launch_decode_hd(const void* qkv, const void* kv, int64_t seq_stride, int B, int H,
-                            const int32_t* pos0, int max_keys, float* part, void* out, hipStream_t s) {
-    const int d = H * HD;
-    const int nsplit = (max_keys + DEC_KEYS - 1) / DEC_KEYS;
-    hipLaunchKernelGGL((decode_attention_kernel<T, HD>), dim3(nsplit, H, B), dim3(256), 0, s, (const T*)qkv,
-                       (const T*)kv, seq_stride, d, pos0, part, nsplit);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((decode_combine_kernel<T, HD>), dim3(H, B), dim3(HD), 0, s, part, nsplit, pos0, d,
-                       (T*)out);
+                            const int32_t* pos0, void* out, hipStream_t s) {
+    // 16 waves for 64-dim heads; 8 for 128 (twice the load registers per chunk)
+    constexpr int NW = HD == 64 ? 16 : 8;
+    hipLaunchKernelGGL((decode_attention_kernel<T, HD, NW>), dim3(H, B), dim3(64 * NW), 0, s, (const T*)qkv,
+                       (const T*)kv, seq_stride, H * HD, pos0, (T*)out);
     return hipGetLastError();
 }
 }  // namespace
@@ -429,21 +429,16 @@ hipError_t launch_attention(int dtype, const void* qkv, void* out, int B, int T_
                                T_len, H, hd, s);
 }
 
-size_t decode_attention_part_floats(int B, int H, int hd, int max_keys) {
-    return (size_t)B * H * ((max_keys + DEC_KEYS - 1) / DEC_KEYS) * (hd + 2);
-}
-
 hipError_t launch_decode_attention(int dtype, const void* qkv, const void* kv, int64_t seq_stride,
-                                   int B, int H, int hd, const int32_t* pos0, int max_keys, float* part,
-                                   void* out, hipStream_t s) {
+                                   int B, int H, int hd, const int32_t* pos0, void* out, hipStream_t s) {
     if (B <= 0) return hipSuccess;
-    if (max_keys <= 0 || !pos0) return hipErrorInvalidValue;
+    if (!pos0) return hipErrorInvalidValue;
     if (dtype == 1) {
-        if (hd == 64) return launch_decode_hd<_Float16, 64>(qkv, kv, seq_stride, B, H, pos0, max_keys, part, out, s);
-        if (hd == 128) return launch_decode_hd<_Float16, 128>(qkv, kv, seq_stride, B, H, pos0, max_keys, part, out, s);
+        if (hd == 64) return launch_decode_hd<_Float16, 64>(qkv, kv, seq_stride, B, H, pos0, out, s);
+        if (hd == 128) return launch_decode_hd<_Float16, 128>(qkv, kv, seq_stride, B, H, pos0, out, s);
     } else {
-        if (hd == 64) return launch_decode_hd<__bf16, 64>(qkv, kv, seq_stride, B, H, pos0, max_keys, part, out, s);
-        if (hd == 128) return launch_decode_hd<__bf16, 128>(qkv, kv, seq_stride, B, H, pos0, max_keys, part, out, s);
+        if (hd == 64) return launch_decode_hd<__bf16, 64>(qkv, kv, seq_stride, B, H, pos0, out, s);
+        if (hd == 128) return launch_decode_hd<__bf16, 128>(qkv, kv, seq_stride, B, H, pos0, out, s);
     }
     return hipErrorInvalidValue;
 }

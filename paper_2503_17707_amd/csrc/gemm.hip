@@ -496,23 +496,24 @@ hipError_t launch_typed(int role, const GemmParams& p, const GemmWorkspace& wsp,
 }
 
 // ---- few rows (decode steps): weight streaming without tiles ---------------
-// Each wave owns four consecutive output features n0..n0+3 and walks K in
-// 512-element chunks (lane i takes elements 8i..8i+7 of a chunk, so a row's
-// chunk is one contiguous 1 KiB read), accumulating all MR token rows at once
-// (MR <= 8: the rows of X are re-read from cache by every wave); then the LoRA
-// K2 columns of the tile's group the same way, a wave sum per output, and lane
-// 0 applies the usual epilogue to the four features of each token.
-constexpr int GEMV_MAX_M = 8;
-
+// A block owns four consecutive output features n0..n0+3; its four waves
+// split K (and the LoRA K2 columns) into four equal contiguous parts, so a
+// matrix of N features is streamed by N / 4 blocks and every CU has many
+// waves' loads in flight.  In a part, lane i takes elements 8i..8i+7 of each
+// 512-element chunk (a feature's chunk is one contiguous 1 KiB read), two
+// chunks per step, accumulating all MR token rows at once (MR <= GEMV_MAX_ROWS: the rows
+// of X are re-read from cache by every wave).  Each wave sums its lanes, the
+// four parts are added in wave order through LDS, and the usual epilogue is
+// applied to the four features of each token.
 template <typename T, int MR>
 __device__ __forceinline__ void gemv_dot(const T* __restrict__ X, int64_t ldx, const T* __restrict__ W,
-                                         int64_t ldw, int n0, int M, int K, int lane,
+                                         int64_t ldw, int n0, int M, int kb, int ke, int lane,
                                          float (&acc)[4][MR]) {
-    for (int c0 = lane * 8; c0 < K; c0 += 2 * 512) {
+    for (int c0 = kb + lane * 8; c0 < ke; c0 += 2 * 512) {
         u32x4 wr[2][4], xr[2][MR];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-            const int c = min(c0 + u * 512, K - 8);
+            const int c = min(c0 + u * 512, ke - 8);  // in bounds; the excess is not accumulated
 #pragma unroll
             for (int r = 0; r < 4; ++r) wr[u][r] = *(const u32x4*)(W + (int64_t)(n0 + r) * ldw + c);
 #pragma unroll
@@ -520,7 +521,7 @@ __device__ __forceinline__ void gemv_dot(const T* __restrict__ X, int64_t ldx, c
         }
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-            if (c0 + u * 512 >= K) break;  // wave-uniform
+            if (c0 + u * 512 >= ke) break;
 #pragma unroll
             for (int m = 0; m < MR; ++m) {
                 T xe[8];
@@ -539,20 +540,22 @@ __device__ __forceinline__ void gemv_dot(const T* __restrict__ X, int64_t ldx, c
 
 template <typename T, int EPI, int MR>
 __global__ __launch_bounds__(256) void gemv_kernel(GemmParams p) {
+    __shared__ float part[4][4][MR];  // [wave][feature][token]
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int n0 = (blockIdx.x * 4 + wave) * 4;
-    if (n0 >= p.N) return;  // wave-uniform; no barriers below
+    const int n0 = blockIdx.x * 4;
     float acc[4][MR];
 #pragma unroll
     for (int r = 0; r < 4; ++r)
 #pragma unroll
         for (int m = 0; m < MR; ++m) acc[r][m] = 0.f;
-    gemv_dot<T, MR>((const T*)p.X, p.ldx, (const T*)p.W, p.ldw, n0, p.M, p.K1, lane, acc);
+    const int q1 = p.K1 / 4;  // K1, K2 are multiples of 64: the parts are multiples of 16
+    gemv_dot<T, MR>((const T*)p.X, p.ldx, (const T*)p.W, p.ldw, n0, p.M, wave * q1, (wave + 1) * q1, lane, acc);
     if (p.K2 > 0) {
         const int g = n0 / p.group;
+        const int q2 = p.K2 / 4;
         if ((p.k2_mask >> g) & 1u)
             gemv_dot<T, MR>((const T*)p.X2 + (int64_t)g * p.x2_group_stride, p.ldx2, (const T*)p.W2, p.ldw2, n0,
-                            p.M, p.K2, lane, acc);
+                            p.M, wave * q2, (wave + 1) * q2, lane, acc);
     }
 #pragma unroll
     for (int r = 0; r < 4; ++r)
@@ -560,13 +563,22 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemmParams p) {
         for (int m = 0; m < MR; ++m) acc[r][m] = wave_sum(acc[r][m]);
     if (lane == 0)
 #pragma unroll
-        for (int m = 0; m < MR; ++m)
-            if (m < p.M) epilogue4<T, EPI>(p, m, n0, f32x4{acc[0][m], acc[1][m], acc[2][m], acc[3][m]});
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int m = 0; m < MR; ++m) part[wave][r][m] = acc[r][m];
+    __syncthreads();
+    const int m = threadIdx.x;
+    if (m < MR && m < p.M) {
+        f32x4 v;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = ((part[0][r][m] + part[1][r][m]) + part[2][r][m]) + part[3][r][m];
+        epilogue4<T, EPI>(p, m, n0, v);
+    }
 }
 
 template <typename T, int EPI>
 hipError_t launch_gemv(const GemmParams& p, hipStream_t s) {
-    const dim3 grid((p.N / 4 + 3) / 4);
+    const dim3 grid(p.N / 4);
 #define PB_GEMV(MR) hipLaunchKernelGGL((gemv_kernel<T, EPI, MR>), grid, dim3(256), 0, s, p)
     if (p.M <= 1) PB_GEMV(1);
     else if (p.M <= 2) PB_GEMV(2);
@@ -600,7 +612,7 @@ hipError_t launch_gemm(int dtype, int role, int epi, const GemmParams& p, const 
         return hipErrorInvalidValue;
     const int expect[5] = {EPI_QKV, EPI_RESID, EPI_RELU, EPI_RESID, EPI_SHRINK};
     if (role < 0 || role > 4 || expect[role] != epi) return hipErrorInvalidValue;
-    if (p.M <= GEMV_MAX_M && PB_GEMM_GEMV)
+    if (p.M <= GEMV_MAX_ROWS && PB_GEMM_GEMV)
         return dtype == 1 ? launch_gemv_typed<_Float16>(role, p, s) : launch_gemv_typed<__bf16>(role, p, s);
     if (dtype == 1) return launch_typed<_Float16>(role, p, wsp, s);
     return launch_typed<__bf16>(role, p, wsp, s);

@@ -49,6 +49,10 @@ struct GemmWorkspace {
     size_t bytes;
 };
 
+// Products with at most this many token rows stream the weights with the
+// GEMV kernel (decode steps) instead of MFMA tiles.
+constexpr int GEMV_MAX_ROWS = 8;
+
 // role: 0 qkv, 1 o, 2 fc1, 3 fc2, 4 shrink (selects the instantiation; each
 // role has its own kernel symbol so profiles separate them).  Requires every
 // operand offset (rows * leading dimension) to fit in 31 bits.
@@ -77,14 +81,10 @@ hipError_t launch_kv_store(int dtype, const void* qkv, int n_rows, int T_len, co
 
 // One new query per (sequence, head) of qkv ([B, 3d], q pre-scaled) against
 // cache positions 0 .. *pos0 of kv ([B][seq_stride], rows [k | v] of 2d), the
-// last one the new token's own; out [B, d].  The grid covers max_keys keys
-// whatever *pos0 holds (blocks past the live keys leave at once), so one
-// launch serves every step.  part: scratch of
-// decode_attention_part_floats(B, H, hd, max_keys).
-size_t decode_attention_part_floats(int B, int H, int hd, int max_keys);
+// last one the new token's own; out [B, d].  The launch does not depend on
+// *pos0, so one recorded launch serves every step.
 hipError_t launch_decode_attention(int dtype, const void* qkv, const void* kv, int64_t seq_stride,
-                                   int B, int H, int hd, const int32_t* pos0, int max_keys, float* part,
-                                   void* out, hipStream_t s);
+                                   int B, int H, int hd, const int32_t* pos0, void* out, hipStream_t s);
 
 // out[r, :] = LN(x[r * in_mul + in_add, :]) * g + b, fp32 statistics;
 // out_f32 selects a float output, otherwise dt.

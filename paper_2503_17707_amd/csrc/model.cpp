@@ -169,7 +169,7 @@ struct ArenaLayout {
     int rs, kw;  // LoRA slot width (rank rounded up to 8) and packed width (multiple of 64)
     size_t globals, layers, layer_bytes, loraA, loraB, loraA_layer, loraB_layer;
     size_t x, u, qkv, attn, h, z, rowslot, tokens, slotscale, zf, logits, outtok, staging, ws;
-    size_t kv, kv_layer, kv_seq, dec_part;  // KV cache (elements per layer, per sequence) and decode scratch
+    size_t kv, kv_layer, kv_seq;  // KV cache (elements per layer, per sequence)
     size_t pval, pidx;
     size_t staging_bytes, ws_bytes, total;
 };
@@ -214,9 +214,6 @@ ArenaLayout arena_layout(const pb_config* c) {
     a.kv_seq = c->max_new_tokens > 0 ? (size_t)c->max_pos * 2 * d : 0;
     a.kv_layer = (size_t)B * a.kv_seq;
     a.kv = take(L * a.kv_layer * 2);
-    a.dec_part = take(c->max_new_tokens > 0
-                          ? pb::decode_attention_part_floats((int)B, c->n_heads, (int)(d / c->n_heads), c->max_pos) * 4
-                          : 0);
     a.ws_bytes = gemm_ws_bytes(c);
     a.ws = take(a.ws_bytes);
     a.total = align_up(p, ALIGN);
@@ -789,8 +786,10 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
     const bool qkv_lora = use_lora && (lora_union & (PB_LORA_Q | PB_LORA_K | PB_LORA_V));
     const bool o_lora = use_lora && (lora_union & PB_LORA_O);
     // For few tokens the q/k/v LoRA shrink rides on the kernel that writes the
-    // LayerNorm rows (row-wise dot products); for many it is a GEMM.
-    const bool fuse_shrink = qkv_lora && N <= ROW_SHRINK_MAX_TOKENS;
+    // LayerNorm rows (row-wise dot products); for many it is a GEMM, and for a
+    // handful (decode steps) a GEMV, whose blocks share the A reads that one
+    // LayerNorm block per row would make alone.
+    const bool fuse_shrink = qkv_lora && N > pb::GEMV_MAX_ROWS && N <= ROW_SHRINK_MAX_TOKENS;
     auto row_shrink_args = [&](int layer) {
         pb::RowShrink sh{};
         if (fuse_shrink) {
@@ -851,8 +850,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
                 HIP_TRY(pb::launch_attention(dt, qkv, attn, B, T, H, hd, s));
             } else {
                 const char* kvl = m->at(a.kv) + (size_t)l * a.kv_layer * 2;
-                HIP_TRY(pb::launch_decode_attention(dt, qkv, kvl, (int64_t)a.kv_seq, B, H, hd, pos0, c.max_pos,
-                                                    (float*)m->at(a.dec_part), attn, s));
+                HIP_TRY(pb::launch_decode_attention(dt, qkv, kvl, (int64_t)a.kv_seq, B, H, hd, pos0, attn, s));
             }
         }
         if (o_lora) {

@@ -17,10 +17,15 @@ CASES = {
                             vocab=1000, max_pos=128, dtype="f16", batch=3, seq_len=37,
                             lora_targets=("q", "k", "v", "o"), lora_rank=8, lora_alpha=16.0,
                             n_adapters=2, adapter_of_seq=(0, -1, 1)),
-    # bf16, head_dim 128, a prompt long enough for several key splits of 256
+    # bf16, head_dim 128, a prompt longer than one pass of the block's waves
+    # over the keys (8 waves x 64 keys)
     "hd128": synth.Workload(name="hd128", seed=32, n_layers=2, d_model=256, n_heads=2, d_ffn=384,
-                            vocab=777, max_pos=640, dtype="bf16", batch=2, seq_len=300,
+                            vocab=777, max_pos=640, dtype="bf16", batch=2, seq_len=560,
                             lora_targets=("q", "v"), lora_rank=16, lora_alpha=32.0, n_adapters=1),
+    # f16, head_dim 64, past one pass of 16 waves x 64 keys
+    "long64": synth.Workload(name="long64", seed=33, n_layers=2, d_model=128, n_heads=2, d_ffn=256,
+                             vocab=500, max_pos=1040, dtype="f16", batch=1, seq_len=1030,
+                             lora_targets=("q", "k", "v", "o"), lora_rank=8, lora_alpha=8.0, n_adapters=1),
 }
 STEPS = 4
 
