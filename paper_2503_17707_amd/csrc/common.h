@@ -75,6 +75,14 @@ template <typename T> __device__ inline u32x2 pack4(float a, float b, float c, f
     return r;
 }
 
+// Barrier for exchanges through LDS only: the fences order LDS accesses
+// (waiting for LDS, not for outstanding global stores as __syncthreads does).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ inline float wave_sum(float v) {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
     return v;

@@ -93,8 +93,12 @@ __device__ __forceinline__ void epilogue4(const GemmParams& p, int m, int n, f32
         float sc[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) sc[r] = n + r < p.qcols ? p.qscale : 1.f;
-        *(u32x2*)((T*)p.C + (int64_t)m * p.ldc + n) =
-            pack4<T>(y[0] * sc[0], y[1] * sc[1], y[2] * sc[2], y[3] * sc[3]);
+        const u32x2 out = pack4<T>(y[0] * sc[0], y[1] * sc[1], y[2] * sc[2], y[3] * sc[3]);
+        *(u32x2*)((T*)p.C + (int64_t)m * p.ldc + n) = out;
+        if (p.kv && n >= p.qcols) {  // qcols is a multiple of 4: the group is all key or all value
+            const int64_t row = (int64_t)(m / p.kv_T) * p.kv_seq + (int64_t)(*p.kv_pos + m % p.kv_T) * 2 * p.qcols;
+            *(u32x2*)((T*)p.kv + row + (n - p.qcols)) = out;
+        }
     } else if (EPI == EPI_RELU) {
         *(u32x2*)((T*)p.C + (int64_t)m * p.ldc + n) =
             pack4<T>(fmaxf(y[0], 0.f), fmaxf(y[1], 0.f), fmaxf(y[2], 0.f), fmaxf(y[3], 0.f));
@@ -318,27 +322,40 @@ __global__ __launch_bounds__(256) void splitk_resid_ln_kernel(GemmParams p, Spli
     const int64_t stride = (int64_t)p.M * p.N;
     float* xr = p.R + (int64_t)m * p.ldr;
     const float* wr = sa.ws + (int64_t)m * p.N;
-    f32x4 v[MAXC];
+    // every load of every chunk first (the stores to R below would otherwise
+    // order the next chunk's loads behind them), then sums and stores; with
+    // few chunks the loads are unconditional, a chunk past nc re-reading the
+    // last one, so that no branch splits them into batches
+    constexpr int NL = NS > 0 ? NS : 1;
+    f32x4 v[MAXC], w[MAXC][NL];
+    u32x2 braw[MAXC];
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i) {
+        int c = threadIdx.x + 256 * i;
+        if (MAXC <= 4) c = min(c, nc - 1);
+        else if (c >= nc) continue;
+#pragma unroll
+        for (int s = 0; s < NL; ++s) w[i][s] = *(const f32x4*)(wr + s * stride + 4 * c);
+        braw[i] = *(const u32x2*)((const T*)p.bias + 4 * c);
+        v[i] = *(const f32x4*)(xr + 4 * c);
+    }
     float sum = 0.f;
 #pragma unroll
     for (int i = 0; i < MAXC; ++i) {
         const int c = threadIdx.x + 256 * i;
         if (c < nc) {
-            f32x4 w[NS > 0 ? NS : 1];
+            f32x4 a = w[i][0];
 #pragma unroll
-            for (int s = 0; s < (NS > 0 ? NS : 1); ++s) w[s] = *(const f32x4*)(wr + s * stride + 4 * c);
-            const u32x2 braw = *(const u32x2*)((const T*)p.bias + 4 * c);
-            f32x4 x = *(const f32x4*)(xr + 4 * c);
-            f32x4 a = w[0];
-#pragma unroll
-            for (int s = 1; s < NS; ++s) a = f32x4{a[0] + w[s][0], a[1] + w[s][1], a[2] + w[s][2], a[3] + w[s][3]};
+            for (int s = 1; s < NS; ++s)
+                a = f32x4{a[0] + w[i][s][0], a[1] + w[i][s][1], a[2] + w[i][s][2], a[3] + w[i][s][3]};
             if (NS == 0)
                 for (int s = 1; s < sa.splits; ++s) {
                     const f32x4 u = *(const f32x4*)(wr + s * stride + 4 * c);
                     a = f32x4{a[0] + u[0], a[1] + u[1], a[2] + u[2], a[3] + u[3]};
                 }
             T bb[4];
-            __builtin_memcpy(bb, &braw, 8);
+            __builtin_memcpy(bb, &braw[i], 8);
+            f32x4 x = v[i];
 #pragma unroll
             for (int r = 0; r < 4; ++r) x[r] += a[r] + (float)bb[r];
             *(f32x4*)(xr + 4 * c) = x;

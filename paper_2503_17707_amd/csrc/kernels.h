@@ -33,6 +33,10 @@ struct GemmParams {
     void* C; int64_t ldc;
     float* R; int64_t ldr;
     float qscale; int qcols;
+    // Optional KV-cache write (EPI_QKV): the key and value columns [qcols,
+    // 3 qcols) of token row m also go to cache row (m / kv_T) * kv_seq +
+    // (*kv_pos + m % kv_T) * 2 qcols, laid out [k | v] (kv NULL = none).
+    void* kv; const int32_t* kv_pos; int kv_T; int64_t kv_seq;
     const int32_t* row_slot; const float* slot_scale; int slot_width; int kw;
     // Optional LayerNorm fused after a residual epilogue (EPI_RESID with N the
     // model width): when the launcher splits K, its row-wise reduce also writes
@@ -73,11 +77,6 @@ hipError_t launch_attention_kv(int dtype, const void* qkv, const void* kv, int64
 // can move it.
 hipError_t launch_embed(int dtype, const int32_t* tok, const void* E, const void* P, float* x,
                         int n_rows, int T, int d, const int32_t* pos0, hipStream_t s);
-
-// Keys and values of n_rows token rows of qkv into the KV cache at positions
-// *pos0 + t (see misc.hip).
-hipError_t launch_kv_store(int dtype, const void* qkv, int n_rows, int T_len, const int32_t* pos0, int d,
-                           void* kv, int64_t seq_stride, hipStream_t s);
 
 // One new query per (sequence, head) of qkv ([B, 3d], q pre-scaled) against
 // cache positions 0 .. *pos0 of kv ([B][seq_stride], rows [k | v] of 2d), the

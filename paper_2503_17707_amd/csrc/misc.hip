@@ -292,32 +292,6 @@ hipError_t launch_embed(int dtype, const int32_t* tok, const void* E, const void
     return hipGetLastError();
 }
 
-// ---- KV cache: keys and values of token rows into their cache positions ----
-// Row r of qkv ([N, 3d], sequence-major, T_len rows per sequence) holds the
-// key at columns [d, 2d) and the value at [2d, 3d); they go to cache row
-// (sequence r / T_len, position *pos0 + r % T_len) of kv ([B][seq_rows][2d]).
-template <typename T>
-__global__ __launch_bounds__(256) void kv_store_kernel(const T* __restrict__ qkv, int d, int T_len,
-                                                      const int32_t* __restrict__ pos0, T* __restrict__ kv,
-                                                      int64_t seq_stride) {
-    const int r = blockIdx.x;
-    const T* src = qkv + (int64_t)r * 3 * d + d;
-    T* dst = kv + (int64_t)(r / T_len) * seq_stride + (int64_t)(*pos0 + r % T_len) * 2 * d;
-    for (int c = threadIdx.x * 8; c < 2 * d; c += 256 * 8) *(u32x4*)(dst + c) = *(const u32x4*)(src + c);
-}
-
-hipError_t launch_kv_store(int dtype, const void* qkv, int n_rows, int T_len, const int32_t* pos0, int d,
-                           void* kv, int64_t seq_stride, hipStream_t s) {
-    if (n_rows <= 0) return hipSuccess;
-    if (dtype == 1)
-        hipLaunchKernelGGL(kv_store_kernel<_Float16>, dim3(n_rows), dim3(256), 0, s,
-                           (const _Float16*)qkv, d, T_len, pos0, (_Float16*)kv, seq_stride);
-    else
-        hipLaunchKernelGGL(kv_store_kernel<__bf16>, dim3(n_rows), dim3(256), 0, s,
-                           (const __bf16*)qkv, d, T_len, pos0, (__bf16*)kv, seq_stride);
-    return hipGetLastError();
-}
-
 hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t in_add,
                             const void* g, const void* b, void* out, bool out_f32, int rows,
                             int d, float eps, hipStream_t s, const RowShrink* shp) {

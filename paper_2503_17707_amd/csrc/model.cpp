@@ -834,11 +834,11 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             p.bias = m->ltensor(l, PB_T_BQ);
             p.C = qkv; p.ldc = 3 * d;
             p.qscale = 1.0f / std::sqrt((float)hd); p.qcols = d;
+            if (a.kv_layer && !reuse_kv) {  // keys and values of the new tokens into the cache
+                p.kv = m->at(a.kv) + (size_t)l * a.kv_layer * 2;
+                p.kv_pos = pos0; p.kv_T = T; p.kv_seq = (int64_t)a.kv_seq;
+            }
             HIP_TRY(pb::launch_gemm(dt, 0, pb::EPI_QKV, p, gws, s));
-        }
-        if (a.kv_layer && !reuse_kv) {  // keys and values of the new tokens into the cache
-            char* kvl = m->at(a.kv) + (size_t)l * a.kv_layer * 2;
-            HIP_TRY(pb::launch_kv_store(dt, qkv, N, T, pos0, d, kvl, (int64_t)a.kv_seq, s));
         }
         {
             Timed t(m, PB_K_ATTN);

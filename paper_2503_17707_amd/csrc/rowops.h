@@ -24,9 +24,9 @@ struct RowShrink {
 __device__ __forceinline__ float block_sum256(float v, float* red) {
     v = wave_sum(v);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    __syncthreads();  // previous use of red finished
+    lds_barrier();  // previous use of red finished
     if (lane == 0) red[wave] = v;
-    __syncthreads();
+    lds_barrier();
     return (red[0] + red[1]) + (red[2] + red[3]);
 }
 
@@ -163,9 +163,9 @@ __device__ __forceinline__ void row_shrink(const RowShrink& sh, int m, int d, co
                 }
             }
             const float tot = wave_sum16(part, lane);
-            __syncthreads();  // previous use of red finished
+            lds_barrier();  // previous use of red finished
             if ((lane & 3) == 0) red[wave][o_lane] = tot;
-            __syncthreads();
+            lds_barrier();
             if (tid < 16 && j0 + tid < sh.rs) {
                 const float zsum = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
                 zr[t * sh.kw + slot * sh.rs + j0 + tid] = (T)(scale * zsum);
