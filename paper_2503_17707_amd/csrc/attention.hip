@@ -272,7 +272,7 @@ hipError_t launch_hd(const void* qkv, const void* kv, int64_t kv_ld, int64_t kv_
         attr_set = true;
     }
     dim3 grid((T_len + 4 * QW - 1) / (4 * QW), H, B);
-    hipLaunchKernelGGL((attention_kernel<T, HD, QW>), grid, dim3(256), LDS, s, (const T*)qkv, (const T*)kv,
+    PB_LAUNCH((attention_kernel<T, HD, QW>), grid, dim3(256), LDS, s, (const T*)qkv, (const T*)kv,
                        kv_ld, kv_seq, (T*)out, T_len, H);
     return hipGetLastError();
 }
@@ -400,7 +400,7 @@ hipError_t launch_decode_hd(const void* qkv, const void* kv, int64_t seq_stride,
                             const int32_t* pos0, void* out, hipStream_t s) {
     // 16 waves for 64-dim heads; 8 for 128 (twice the load registers per chunk)
     constexpr int NW = HD == 64 ? 16 : 8;
-    hipLaunchKernelGGL((decode_attention_kernel<T, HD, NW>), dim3(H, B), dim3(64 * NW), 0, s, (const T*)qkv,
+    PB_LAUNCH((decode_attention_kernel<T, HD, NW>), dim3(H, B), dim3(64 * NW), 0, s, (const T*)qkv,
                        (const T*)kv, seq_stride, H * HD, pos0, (T*)out);
     return hipGetLastError();
 }

@@ -1,6 +1,7 @@
 // Device-side helpers shared by the CDNA4 (gfx950) kernels.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -93,4 +94,26 @@ __device__ inline float wave_max(float v) {
     return v;
 }
 
+// Timing of a span of launches by events taken from the kernels' own dispatch
+// packets (no marker packets between kernels): while `stop` is set, the next
+// launch records `start` as it begins and every launch records `stop` as it
+// ends, so the span runs from the first kernel's start to the last one's end.
+struct LaunchTiming {
+    hipEvent_t start, stop;
+};
+extern thread_local LaunchTiming g_launch_timing;
+
 }  // namespace pb
+
+// Every kernel launch of the library (a plain launch unless a span is timed).
+#define PB_LAUNCH(kernel, grid, block, shmem, stream, ...)                                  \
+    do {                                                                                    \
+        if (::pb::g_launch_timing.stop) {                                                   \
+            const hipEvent_t pb_start_ = ::pb::g_launch_timing.start;                       \
+            ::pb::g_launch_timing.start = nullptr;                                          \
+            hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, pb_start_,            \
+                                  ::pb::g_launch_timing.stop, 0, __VA_ARGS__);              \
+        } else {                                                                            \
+            hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);            \
+        }                                                                                   \
+    } while (0)

@@ -374,7 +374,7 @@ __global__ __launch_bounds__(256) void splitk_resid_ln_kernel(GemmParams p, Spli
 template <typename T, int ROLE>
 hipError_t launch_resid_ln(const GemmParams& p, const SplitArgs& sa, hipStream_t s) {
 #define PB_RLN(MAXC, NS) \
-    hipLaunchKernelGGL((splitk_resid_ln_kernel<T, ROLE, MAXC, NS>), dim3(p.M), dim3(256), 0, s, p, sa)
+    PB_LAUNCH((splitk_resid_ln_kernel<T, ROLE, MAXC, NS>), dim3(p.M), dim3(256), 0, s, p, sa)
     // few rows (latency-bound): every partial in flight at once; many rows:
     // occupancy hides the latency and registers matter more
     if (p.N <= 2048) {
@@ -416,7 +416,7 @@ hipError_t finish_split(const GemmParams& p, const SplitArgs& sa, hipStream_t s)
         return e;
     }
     const int64_t groups = (int64_t)p.M * (p.N / 4);
-    hipLaunchKernelGGL((splitk_reduce_kernel<T, EPI, ROLE>), dim3((unsigned)((groups + 255) / 256)), dim3(256), 0,
+    PB_LAUNCH((splitk_reduce_kernel<T, EPI, ROLE>), dim3((unsigned)((groups + 255) / 256)), dim3(256), 0,
                        s, p, sa);
     return hipGetLastError();
 }
@@ -433,7 +433,7 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, int splits,
     }
     const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
     const SplitArgs sa = make_split(p, wsp, splits);
-    hipLaunchKernelGGL((gemm_kernel<T, EPI, BM, BN, WGM, WGN, ROLE, S>), dim3(tiles * sa.splits),
+    PB_LAUNCH((gemm_kernel<T, EPI, BM, BN, WGM, WGN, ROLE, S>), dim3(tiles * sa.splits),
                        dim3(64 * WGM * WGN), LDS, s, p, sa);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess || sa.splits == 1) return e;
@@ -596,7 +596,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemmParams p) {
 template <typename T, int EPI>
 hipError_t launch_gemv(const GemmParams& p, hipStream_t s) {
     const dim3 grid(p.N / 4);
-#define PB_GEMV(MR) hipLaunchKernelGGL((gemv_kernel<T, EPI, MR>), grid, dim3(256), 0, s, p)
+#define PB_GEMV(MR) PB_LAUNCH((gemv_kernel<T, EPI, MR>), grid, dim3(256), 0, s, p)
     if (p.M <= 1) PB_GEMV(1);
     else if (p.M <= 2) PB_GEMV(2);
     else if (p.M <= 4) PB_GEMV(4);

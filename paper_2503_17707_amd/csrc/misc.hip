@@ -7,6 +7,8 @@
 
 namespace pb {
 
+thread_local LaunchTiming g_launch_timing = {nullptr, nullptr};
+
 namespace {
 
 // ---- embedding: OPT learned absolute positions, no offset -------------------
@@ -284,10 +286,10 @@ hipError_t launch_embed(int dtype, const int32_t* tok, const void* E, const void
                         int n_rows, int T_len, int d, const int32_t* pos0, hipStream_t s) {
     if (n_rows <= 0) return hipSuccess;
     if (dtype == 1)
-        hipLaunchKernelGGL(embed_kernel<_Float16>, dim3(n_rows), dim3(256), 0, s, tok,
+        PB_LAUNCH(embed_kernel<_Float16>, dim3(n_rows), dim3(256), 0, s, tok,
                            (const _Float16*)E, (const _Float16*)P, x, T_len, d, pos0);
     else
-        hipLaunchKernelGGL(embed_kernel<__bf16>, dim3(n_rows), dim3(256), 0, s, tok,
+        PB_LAUNCH(embed_kernel<__bf16>, dim3(n_rows), dim3(256), 0, s, tok,
                            (const __bf16*)E, (const __bf16*)P, x, T_len, d, pos0);
     return hipGetLastError();
 }
@@ -300,7 +302,7 @@ hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t i
     RowShrink sh{};
     if (shp && !out_f32) sh = *shp;
 #define PB_LN1(T, F, C)                                                                            \
-    hipLaunchKernelGGL((layernorm_kernel<T, F, C>), dim3(rows), dim3(256), 0, s, x, in_mul, in_add, \
+    PB_LAUNCH((layernorm_kernel<T, F, C>), dim3(rows), dim3(256), 0, s, x, in_mul, in_add, \
                        (const T*)g, (const T*)b, out, d, eps, sh)
 #define PB_LN(T, F)                                                                                \
     do {                                                                                           \
@@ -329,7 +331,7 @@ hipError_t launch_lm_head(int dtype, const float* z, int B, const void* E, int V
     for (int b0 = 0; b0 < B; b0 += 4) {
         const int nb = std::min(4, B - b0);
 #define PB_LM(T, NB)                                                                           \
-    hipLaunchKernelGGL((lm_head_kernel<T, NB>), dim3(blocks), dim3(256), 0, s, z, b0,          \
+    PB_LAUNCH((lm_head_kernel<T, NB>), dim3(blocks), dim3(256), 0, s, z, b0,          \
                        (const T*)E, V, d, logits, pval, pidx, blocks)
         if (dtype == 1) {
             if (nb == 1) PB_LM(_Float16, 1); else if (nb == 2) PB_LM(_Float16, 2);
@@ -348,7 +350,7 @@ hipError_t launch_lm_head(int dtype, const float* z, int B, const void* E, int V
 hipError_t launch_argmax(const float* pval, const int* pidx, int B, int V, int32_t* tok,
                          hipStream_t s) {
     if (B <= 0) return hipSuccess;
-    hipLaunchKernelGGL(argmax_final_kernel, dim3(B), dim3(256), 0, s, pval, pidx,
+    PB_LAUNCH(argmax_final_kernel, dim3(B), dim3(256), 0, s, pval, pidx,
                        lm_head_blocks(V), tok);
     return hipGetLastError();
 }
@@ -359,11 +361,11 @@ hipError_t launch_lora_pack(int dtype, const void* staging, size_t staging_layer
     if (L <= 0) return hipSuccess;
     dim3 grid(L, 4, 2);
     if (dtype == 1)
-        hipLaunchKernelGGL(lora_pack_kernel<_Float16>, grid, dim3(256), 0, s,
+        PB_LAUNCH(lora_pack_kernel<_Float16>, grid, dim3(256), 0, s,
                            (const _Float16*)staging, staging_layer_elems, d, r, mask, slot, rs, kw,
                            (_Float16*)Acat, (_Float16*)Bcat);
     else
-        hipLaunchKernelGGL(lora_pack_kernel<__bf16>, grid, dim3(256), 0, s, (const __bf16*)staging,
+        PB_LAUNCH(lora_pack_kernel<__bf16>, grid, dim3(256), 0, s, (const __bf16*)staging,
                            staging_layer_elems, d, r, mask, slot, rs, kw, (__bf16*)Acat,
                            (__bf16*)Bcat);
     return hipGetLastError();
@@ -374,10 +376,10 @@ hipError_t launch_lora_merge(int dtype, void* W, const void* Acat, const void* B
     const int64_t threads = (int64_t)d * (d / 8);
     const dim3 grid((unsigned)((threads + 255) / 256));
     if (dtype == 1)
-        hipLaunchKernelGGL(lora_merge_kernel<_Float16>, grid, dim3(256), 0, s, (_Float16*)W, (const _Float16*)Acat,
+        PB_LAUNCH(lora_merge_kernel<_Float16>, grid, dim3(256), 0, s, (_Float16*)W, (const _Float16*)Acat,
                            (const _Float16*)Bcat, d, kw, rs, slot, scale);
     else
-        hipLaunchKernelGGL(lora_merge_kernel<__bf16>, grid, dim3(256), 0, s, (__bf16*)W, (const __bf16*)Acat,
+        PB_LAUNCH(lora_merge_kernel<__bf16>, grid, dim3(256), 0, s, (__bf16*)W, (const __bf16*)Acat,
                            (const __bf16*)Bcat, d, kw, rs, slot, scale);
     return hipGetLastError();
 }

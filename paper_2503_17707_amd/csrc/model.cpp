@@ -718,7 +718,10 @@ int pb_reset_kernel_timing(pb_model* m) {
 
 namespace {
 
-// Brackets one kernel launch with timing events when timing is enabled.
+// Times the launches of one kernel kind (a GEMM and its split-K reduce, say)
+// when timing is enabled: the events come from the kernels' own dispatch
+// packets (the first launch's start, the last one's end), so the span holds
+// no marker packets of its own.
 struct Timed {
     pb_model* m;
     int kind;
@@ -736,10 +739,15 @@ struct Timed {
         idx = m->tused;
         m->tused += 2;
         m->tkind[idx / 2] = kind;
-        (void)hipEventRecord(m->tev[idx], m->compute);
+        pb::g_launch_timing = {m->tev[idx], m->tev[idx + 1]};
     }
     ~Timed() {
-        if (m->timing) (void)hipEventRecord(m->tev[idx + 1], m->compute);
+        if (!m->timing) return;
+        if (pb::g_launch_timing.start) {  // nothing was launched: an empty span
+            (void)hipEventRecord(m->tev[idx], m->compute);
+            (void)hipEventRecord(m->tev[idx + 1], m->compute);
+        }
+        pb::g_launch_timing = {nullptr, nullptr};
     }
 };
 

@@ -15,11 +15,27 @@
       per kernel, the MFMA work executed and the fraction of SIMD cycles the
       matrix units were busy.
 
+  python -m paper_2503_17707_amd.profsum kernels DIR LABEL
+      DIR from `rocprofv3 --kernel-trace --stats -f csv -d DIR -o bench -- python
+      bench.py ...`: the per-kernel statistics, and the average duration per
+      launch of each kernel kind with its split-K reduce counted in (the unit
+      bench.py times with HIP events).
+
+  python -m paper_2503_17707_amd.profsum traffic FETCH WRITE CAL_FETCH CAL_WRITE LABEL
+      FETCH / WRITE from `rocprofv3 --pmc FETCH_SIZE` / `--pmc WRITE_SIZE -f csv
+      -d DIR -o bench -- python bench.py ...`, CAL_* the same counters over
+      `python bench.py --calibrate-copy-mib 1024` (a plain device copy of
+      1 GiB, three times): each counter is scaled by what it reads for the
+      copy, and the bytes of every dispatch of a kernel kind are divided by
+      that kind's launches.  Ends with the block bench.py reads (bytes per
+      launch, valid while the kernel sources keep the printed hash).
+
 Only reads files; used to write the summaries kept with the profiles.
 """
 import collections
 import csv
 import glob
+import hashlib
 import os
 import re
 import sys
@@ -48,7 +64,12 @@ def kind_of(name):
         return roles[int(re.search(r"splitk_resid_ln_kernelIDF16b?_Li(\d+)E", name).group(1))] + " reduce"
     if "splitk_reduce_kernel" in name:
         return roles[int(re.search(r"splitk_reduce_kernelIDF16b?_Li\d+ELi(\d+)E", name).group(1))] + " reduce"
-    for k in ("attention", "layernorm", "lm_head", "argmax", "embed", "lora_pack"):
+    m = re.search(r"gemv_kernelIDF16b?_Li(\d+)E", name)
+    if m:  # decode steps: named by epilogue (o and fc2 share the residual one)
+        return {0: "gemv_qkv", 1: "gemv_fc1", 2: "gemv_o_fc2", 3: "gemv_shrink"}[int(m.group(1))]
+    if "decode_attention" in name:
+        return "decode_attention"
+    for k in ("attention", "layernorm", "lm_head", "argmax", "embed", "lora_pack", "lora_merge"):
         if k in name:
             return k
     return None
@@ -141,14 +162,100 @@ def mfma(d, label):
     return "\n".join(out)
 
 
+def source_sha256():
+    """Hash of the kernel sources, as bench.py computes it."""
+    here = os.path.dirname(os.path.abspath(__file__))
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(here, "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def _base(kind):
+    return kind[:-len(" reduce")] if kind and kind.endswith(" reduce") else kind
+
+
+def kernels(d, label):
+    rows = list(csv.DictReader(open(_one(d, "*kernel_stats.csv"))))
+    out = ["# Kernel durations, %s\n" % label,
+           "Kernel sources (paper_2503_17707_amd/csrc/*) sha256: `%s`\n" % source_sha256(),
+           "| kernel | kind | calls | avg us | total ms | % |", "|---|---|---|---|---|---|"]
+    total, launches = collections.defaultdict(float), collections.defaultdict(int)
+    for r in rows:
+        k = kind_of(r["Name"])
+        if len(out) < 26:
+            out.append("| `%s` | %s | %s | %.2f | %.2f | %.2f |" % (
+                r["Name"][:100], k or "-", r["Calls"], float(r["AverageNs"]) / 1e3,
+                float(r["TotalDurationNs"]) / 1e6, float(r["Percentage"])))
+        if k:
+            total[_base(k)] += float(r["TotalDurationNs"])
+            if not k.endswith(" reduce"):
+                launches[k] += int(r["Calls"])
+    out += ["\nAverage duration per launch by kind (a GEMM kind includes its split-K reduce):\n",
+            "| kind | launches | avg us |", "|---|---|---|"]
+    for k in sorted(total):
+        if launches[k]:
+            out.append("| %s | %d | %.2f |" % (k, launches[k], total[k] / launches[k] / 1e3))
+    return "\n".join(out)
+
+
+def _counter(d, name):
+    per = collections.defaultdict(list)
+    for r in csv.DictReader(open(_one(d, "*counter_collection.csv"))):
+        if r["Counter_Name"].startswith(name):
+            per[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+    return per
+
+
+def traffic(fetch, write, cal_fetch, cal_write, label):
+    f, w = _counter(fetch, "FETCH_SIZE"), _counter(write, "WRITE_SIZE")
+    copy = "__amd_rocclr_copyBuffer"
+    cf = _counter(cal_fetch, "FETCH_SIZE")[copy]
+    cw = _counter(cal_write, "WRITE_SIZE")[copy]
+    kib = 1 << 20  # KiB in the 1 GiB copy
+    sf, sw = kib / (sum(cf) / len(cf)), kib / (sum(cw) / len(cw))
+    out = ["# HBM traffic per kernel launch, %s\n" % label,
+           "FETCH_SIZE and WRITE_SIZE (KiB per dispatch) scaled by what the same counter reads "
+           "for a plain 1 GiB device copy: FETCH_SIZE %.1f KiB -> x%.4f, WRITE_SIZE %.1f KiB -> x%.4f.\n"
+           % (sum(cf) / len(cf), sf, sum(cw) / len(cw), sw),
+           "| kernel | kind | dispatches | read MB / dispatch | write MB / dispatch |", "|---|---|---|---|---|"]
+    tot, launches = collections.defaultdict(float), collections.defaultdict(int)
+    for name, vals in f.items():
+        k = kind_of(name)
+        if not k:
+            continue
+        rb = sum(vals) * 1024 * sf
+        wv = w.get(name, [])
+        wb = sum(wv) * 1024 * sw
+        out.append("| `%s` | %s | %d | %.2f | %.2f |" % (name[:90], k, len(vals), rb / len(vals) / 1e6,
+                                                        (wb / len(wv) if wv else 0.0) / 1e6))
+        tot[_base(k)] += rb + (wb * len(vals) / len(wv) if wv else 0.0)
+        if not k.endswith(" reduce"):
+            launches[k] += len(vals)
+    out += ["\nHBM bytes per launch of each kind (all its dispatches, split-K reduces included, over "
+            "its launches), read by bench.py while the kernel sources keep this hash:\n",
+            "```traffic", "source_sha256 %s" % source_sha256()]
+    for k in sorted(tot):
+        if launches[k]:
+            out.append("%s %.0f" % (k, tot[k] / launches[k]))
+    out.append("```")
+    return "\n".join(out)
+
+
 def main(argv):
-    if len(argv) < 3 or argv[0] not in ("overlap", "mfma") or (argv[0] == "mfma" and len(argv) != 3):
+    usage = {"overlap": (3, 4), "mfma": (3, 3), "kernels": (3, 3), "traffic": (6, 6)}
+    if not argv or argv[0] not in usage or not usage[argv[0]][0] <= len(argv) <= usage[argv[0]][1]:
         raise SystemExit(__doc__)
     if argv[0] == "overlap":
         gap = int(float(argv[3]) * 1e6) if len(argv) > 3 else GAP_NS
         print(overlap(argv[1], argv[2], gap))
-    else:
+    elif argv[0] == "mfma":
         print(mfma(argv[1], argv[2]))
+    elif argv[0] == "kernels":
+        print(kernels(argv[1], argv[2]))
+    else:
+        print(traffic(*argv[1:6]))
 
 
 if __name__ == "__main__":
