@@ -249,7 +249,9 @@ def main():
     t0 = time.perf_counter()
     # room for decode steps after the prompt (none when the prompt fills max_pos)
     dec_steps = max(0, min(args.decode_steps, w.max_pos - w.seq_len))
-    cfg = pb.make_config(w, max_new_tokens=dec_steps)
+    # with a shadow of the unmerged attention weights, so that the merged-LoRA
+    # section can also time an adapter switch
+    cfg = pb.make_config(w, max_new_tokens=dec_steps, merge_shadow=True)
     hw = pb.HostWeights(w, cfg)
     for a in sorted({a for a in w.adapters() if a >= 0}):
         hw.add_lora(a)
@@ -394,7 +396,15 @@ def main():
             m.prefill(toks, base_ad)
         torch.cuda.synchronize(dev)
         ms_m = (time.perf_counter() - t0) / args.steps * 1e3
-        merged = {"slot": used[0], "merge_ms": merge_ms, "ms_per_step": ms_m,
+        # an epoch boundary's switch: restore the shadow, merge again
+        t0 = time.perf_counter()
+        m.merge_lora(used[0])
+        switch_ms = (time.perf_counter() - t0) * 1e3
+        t0 = time.perf_counter()
+        m.unmerge_lora()
+        unmerge_ms = (time.perf_counter() - t0) * 1e3
+        merged = {"slot": used[0], "merge_ms": merge_ms, "switch_ms": switch_ms, "unmerge_ms": unmerge_ms,
+                  "ms_per_step": ms_m,
                   "unmerged_over_merged": ms_step / ms_m,
                   "tokens_equal_unmerged": bool(np.array_equal(mt, first[0])),
                   "max_abs_vs_unmerged": float(np.max(np.abs(ml - first[1])))}

@@ -76,6 +76,9 @@ typedef struct {
     float ln_eps;         /* LayerNorm epsilon (1e-5 for OPT) */
     int32_t max_new_tokens; /* decode steps after a prefill; > 0 keeps a KV cache of
                                [n_layers][max_batch][max_pos][2 d_model] in the arena */
+    int32_t merge_shadow;   /* 1: the arena also keeps a copy of every layer's unmerged
+                               Wq|Wk|Wv|Wo, so merged adapters can be switched and
+                               unmerged on the device (pb_merge_lora, pb_unmerge_lora) */
 } pb_config;
 
 typedef struct pb_model pb_model;
@@ -213,8 +216,42 @@ int pb_plan_loading(int32_t n_layers, int32_t n_gpus, const uint8_t* alive, int3
  * model: every sequence runs with adapter -1 (a prefill or decode naming any
  * adapter fails with PB_ESTATE) and no LoRA work remains on the hot path.
  * pb_stream_layers (or pb_poison_weights) restores the unmerged state.
- * Requires an attached slot and a prior pb_stream_layers (PB_ESTATE). */
+ * With merge_shadow, the first merge after a load copies every layer's
+ * Wq|Wk|Wv|Wo to the shadow, and a merge while another adapter is merged
+ * first restores them from it (an adapter switch: the result is bit-identical
+ * to merging onto freshly streamed weights); without, that merge fails with
+ * PB_ESTATE.  Requires an attached slot and a prior pb_stream_layers
+ * (PB_ESTATE). */
 int pb_merge_lora(pb_model* m, int32_t slot);
+
+/* Restore the unmerged base weights from the shadow copy (blocks until done).
+ * PB_ESTATE when nothing is merged or the model has no merge_shadow. */
+int pb_unmerge_lora(pb_model* m);
+
+/* Epoch-based adapter switching (Section 4.3.2), host side.  Requests are
+ * queued per adapter (0 .. n_adapters-1, or -1 for the base model); a batch
+ * holds requests of one adapter only, oldest first.  With epoch_batches = E >
+ * 0, batches of the active (merged) adapter go first; after E batches of it,
+ * or when its queue is empty, the scheduler moves to the other queue whose
+ * oldest request has waited longest (staying if no other queue has work).
+ * With E = 0 it serves requests in arrival order (the eager baseline: a batch
+ * is a run of consecutive arrivals with one adapter).  pb_sched_next reports
+ * whether the batch needs another adapter merged than the previous one
+ * (`switched`, always 1 for the first batch); the caller merges
+ * (pb_merge_lora) or unmerges before running it.  Calls on one scheduler must
+ * not overlap. */
+typedef struct pb_sched pb_sched;
+int pb_sched_create(int32_t n_adapters, int32_t epoch_batches, pb_sched** out);
+int pb_sched_destroy(pb_sched* s);
+/* PB_EINVAL for an adapter outside [-1, n_adapters). */
+int pb_sched_submit(pb_sched* s, int64_t request_id, int32_t adapter);
+/* Up to max_batch (>= 1) request ids into ids; *n = 0 when every queue is
+ * empty (then *adapter and *switched are left unchanged). */
+int pb_sched_next(pb_sched* s, int32_t max_batch, int64_t* ids, int32_t* n, int32_t* adapter,
+                  int32_t* switched);
+/* Requests still queued, adapter switches so far, the active adapter (-2
+ * before the first batch). */
+int pb_sched_stats(pb_sched* s, int64_t* pending, int64_t* switches, int32_t* active);
 
 /* KV-cache reconstruction after a failure (Section 4.4.2: a request that was
  * decoding is replayed as one prefill over its prompt and the tokens produced

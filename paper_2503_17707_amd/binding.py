@@ -41,7 +41,7 @@ class Config(ctypes.Structure):
                 ("max_tokens", ctypes.c_int32), ("max_batch", ctypes.c_int32),
                 ("max_adapters", ctypes.c_int32), ("max_rank", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("ln_eps", ctypes.c_float),
-                ("max_new_tokens", ctypes.c_int32)]
+                ("max_new_tokens", ctypes.c_int32), ("merge_shadow", ctypes.c_int32)]
 
 
 _SIGS = {
@@ -77,6 +77,15 @@ _SIGS = {
                                      ctypes.POINTER(ctypes.c_float)]),
     "pb_invalidate_kv": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_uint8), ctypes.c_int32]),
     "pb_merge_lora": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
+    "pb_unmerge_lora": (ctypes.c_int, [ctypes.c_void_p]),
+    "pb_sched_create": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_void_p)]),
+    "pb_sched_destroy": (ctypes.c_int, [ctypes.c_void_p]),
+    "pb_sched_submit": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32]),
+    "pb_sched_next": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(ctypes.c_int64),
+                                     ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
+                                     ctypes.POINTER(ctypes.c_int32)]),
+    "pb_sched_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
+                                      ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int32)]),
     "pb_plan_loading": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_uint8),
                                        ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
                                        ctypes.POINTER(ctypes.c_int32)]),
@@ -145,9 +154,10 @@ def check(rc: int) -> None:
 
 def make_config(w, max_tokens: Optional[int] = None, max_batch: Optional[int] = None,
                 max_adapters: Optional[int] = None, max_rank: Optional[int] = None,
-                max_new_tokens: int = 0) -> Config:
+                max_new_tokens: int = 0, merge_shadow: bool = False) -> Config:
     """pb_config of a synth.Workload (capacities default to the workload's own sizes;
-    max_new_tokens > 0 adds a KV cache for decode steps)."""
+    max_new_tokens > 0 adds a KV cache for decode steps; merge_shadow keeps the
+    unmerged attention weights for adapter switching)."""
     return Config(n_layers=w.n_layers, d_model=w.d_model, n_heads=w.n_heads, d_ffn=w.d_ffn,
                   vocab=w.vocab, max_pos=w.max_pos,
                   max_tokens=max_tokens or w.batch * w.seq_len,
@@ -155,7 +165,7 @@ def make_config(w, max_tokens: Optional[int] = None, max_batch: Optional[int] = 
                   max_adapters=w.n_adapters if max_adapters is None else max_adapters,
                   max_rank=max_rank or w.lora_rank,
                   dtype=PB_BF16 if w.dtype == "bf16" else PB_F16, ln_eps=w.ln_eps,
-                  max_new_tokens=max_new_tokens)
+                  max_new_tokens=max_new_tokens, merge_shadow=1 if merge_shadow else 0)
 
 
 def layer_tensor(cfg: Config, name: str):
@@ -395,6 +405,9 @@ class Model:
     def merge_lora(self, slot: int):
         check(lib().pb_merge_lora(self.h, slot))
 
+    def unmerge_lora(self):
+        check(lib().pb_unmerge_lora(self.h))
+
     def invalidate_kv(self, layer_lost: Sequence[bool], value: int = 0xFF):
         lost = np.ascontiguousarray([1 if x else 0 for x in layer_lost], dtype=np.uint8)
         check(lib().pb_invalidate_kv(self.h, lost.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), value))
@@ -458,6 +471,39 @@ def attach_all(m: Model, hw: HostWeights):
     for a in used:
         blobs = hw.loras.get(a) or hw.add_lora(a)
         m.attach_lora(a, blobs, w.lora_rank, w.lora_alpha, hw.lora_mask())
+
+
+class Scheduler:
+    """Epoch-based adapter switching (pb_sched_*): per-adapter request queues;
+    epoch_batches = 0 is the eager, arrival-order baseline."""
+
+    def __init__(self, n_adapters: int, epoch_batches: int):
+        h = ctypes.c_void_p()
+        check(lib().pb_sched_create(n_adapters, epoch_batches, ctypes.byref(h)))
+        self.h = h
+
+    def submit(self, request_id: int, adapter: int):
+        check(lib().pb_sched_submit(self.h, request_id, adapter))
+
+    def next(self, max_batch: int):
+        """(request ids, adapter, switched), or None when every queue is empty."""
+        ids = (ctypes.c_int64 * max_batch)()
+        n, a, sw = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        check(lib().pb_sched_next(self.h, max_batch, ids, ctypes.byref(n), ctypes.byref(a), ctypes.byref(sw)))
+        if n.value == 0:
+            return None
+        return list(ids[:n.value]), a.value, bool(sw.value)
+
+    def stats(self):
+        """(pending, switches, active adapter; -2 before the first batch)."""
+        p, sw, a = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int32()
+        check(lib().pb_sched_stats(self.h, ctypes.byref(p), ctypes.byref(sw), ctypes.byref(a)))
+        return p.value, sw.value, a.value
+
+    def close(self):
+        if self.h:
+            check(lib().pb_sched_destroy(self.h))
+            self.h = None
 
 
 def plan_loading(n_layers: int, alive: Sequence[bool]):

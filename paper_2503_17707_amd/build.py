@@ -15,7 +15,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "lib")
 LIB = os.path.join(OUT_DIR, "libpipeboost.so")
-SOURCES = ["gemm.hip", "attention.hip", "misc.hip", "model.cpp"]
+SOURCES = ["gemm.hip", "attention.hip", "misc.hip", "model.cpp", "sched.cpp"]
 ARCH = os.environ.get("PB_OFFLOAD_ARCH", "gfx950")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH, "-Wall", "-Wno-unused-result",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -44,6 +44,15 @@ int fail(int code, const char* fmt, ...) {
     return code;
 }
 
+}  // namespace
+
+// The same message slot for the library's other host sources (not exported).
+__attribute__((visibility("hidden"))) int pb_fail_status(int code, const char* msg) {
+    return fail(code, "%s", msg);
+}
+
+namespace {
+
 #define HIP_TRY(call)                                                                  \
     do {                                                                               \
         hipError_t e_ = (call);                                                        \
@@ -93,6 +102,7 @@ bool config_ok(const pb_config* c, std::string* why) {
     if (c->max_adapters > 0 && (c->max_rank < 1 || c->max_rank > MAX_RANK))
         return bad("max_rank must be in [1, 64]");
     if (c->max_new_tokens < 0) return bad("max_new_tokens must be >= 0");
+    if (c->merge_shadow != 0 && c->merge_shadow != 1) return bad("merge_shadow must be 0 or 1");
     if (c->dtype != PB_BF16 && c->dtype != PB_F16) return bad("dtype must be PB_BF16 or PB_F16");
     if (!(c->ln_eps > 0.f)) return bad("ln_eps must be > 0");
     return true;
@@ -170,6 +180,7 @@ struct ArenaLayout {
     size_t globals, layers, layer_bytes, loraA, loraB, loraA_layer, loraB_layer;
     size_t x, u, qkv, attn, h, z, rowslot, tokens, slotscale, zf, logits, outtok, staging, ws;
     size_t kv, kv_layer, kv_seq;  // KV cache (elements per layer, per sequence)
+    size_t shadow, shadow_layer, attn_w;  // unmerged Wq|Wk|Wv|Wo copies: bytes per layer; their offset in a layer
     size_t pval, pidx;
     size_t staging_bytes, ws_bytes, total;
 };
@@ -214,6 +225,12 @@ ArenaLayout arena_layout(const pb_config* c) {
     a.kv_seq = c->max_new_tokens > 0 ? (size_t)c->max_pos * 2 * d : 0;
     a.kv_layer = (size_t)B * a.kv_seq;
     a.kv = take(L * a.kv_layer * 2);
+    {
+        const LayerLayout ll = layer_layout(c);
+        a.attn_w = ll.off[PB_T_WQ] * 2;
+        a.shadow_layer = c->merge_shadow ? (ll.off[PB_T_WO] + ll.num[PB_T_WO] - ll.off[PB_T_WQ]) * 2 : 0;
+        a.shadow = take(L * a.shadow_layer);
+    }
     a.ws_bytes = gemm_ws_bytes(c);
     a.ws = take(a.ws_bytes);
     a.total = align_up(p, ALIGN);
@@ -265,6 +282,7 @@ struct pb_model {
     bool ring_busy[STAGE_SLOTS] = {};
     int ring_next = 0;
     int merged_slot = -1;  // adapter merged into the device base weights (-1: none)
+    bool shadow_valid = false;  // the shadow holds this load's unmerged attention weights
     // decode state: sequences of the last prefill, their length so far
     int dec_B = 0, dec_len = 0, dec_steps = 0;
     std::vector<int> dec_adapter;
@@ -608,6 +626,7 @@ int pb_stream_layers(pb_model* m, const int32_t* layer_order, int32_t n_layers,
     HIP_TRY(hipEventRecord(m->ev_load0, m->copy));
     m->last_load_bytes = (double)gb + (double)L * (double)lb;
     m->merged_slot = -1;  // the base weights arrive unmerged
+    m->shadow_valid = false;
     if (all_pinned) {
         // every copy is a DMA from locked pages: enqueue them all now
         const int rc = run_load(m, jobs);
@@ -671,6 +690,7 @@ int pb_poison_weights(pb_model* m, int32_t value) {
     m->streamed = false;
     m->dec_B = 0;
     m->merged_slot = -1;
+    m->shadow_valid = false;
     return PB_OK;
 }
 
@@ -1148,21 +1168,50 @@ extern "C" int pb_plan_loading(int32_t n_layers, int32_t n_gpus, const uint8_t* 
     return PB_OK;
 }
 
+// Copy every layer's Wq|Wk|Wv|Wo between the layer blobs and the shadow (one
+// strided copy on the compute stream).
+static int copy_shadow(pb_model* m, bool to_shadow) {
+    const ArenaLayout& a = m->lay;
+    char* layers = m->at(a.layers) + a.attn_w;
+    char* shadow = m->at(a.shadow);
+    if (to_shadow)
+        HIP_TRY(hipMemcpy2DAsync(shadow, a.shadow_layer, layers, a.layer_bytes, a.shadow_layer, m->cfg.n_layers,
+                                 hipMemcpyDeviceToDevice, m->compute));
+    else
+        HIP_TRY(hipMemcpy2DAsync(layers, a.layer_bytes, shadow, a.shadow_layer, a.shadow_layer, m->cfg.n_layers,
+                                 hipMemcpyDeviceToDevice, m->compute));
+    return PB_OK;
+}
+
 extern "C" int pb_merge_lora(pb_model* m, int32_t slot) {
     if (!m) return fail(PB_EINVAL, "model is NULL");
     const pb_config& c = m->cfg;
     if (slot < 0 || slot >= c.max_adapters) return fail(PB_EINVAL, "slot %d outside [0, %d)", slot, c.max_adapters);
     if (!m->slot_valid[slot]) return fail(PB_ESTATE, "adapter slot %d holds no adapter", slot);
     if (!m->streamed) return fail(PB_ESTATE, "merge before pb_stream_layers");
-    if (m->merged_slot >= 0) return fail(PB_ESTATE, "adapter %d is already merged; stream the base layers again first", m->merged_slot);
+    if (m->merged_slot >= 0 && !c.merge_shadow)
+        return fail(PB_ESTATE, "adapter %d is already merged; stream the base layers again first (or keep a merge shadow)",
+                    m->merged_slot);
     const ArenaLayout& a = m->lay;
     hipStream_t s = m->compute;
     // every layer (and the adapter) must have landed before it is rewritten
     if (m->lora_recorded) HIP_TRY(hipStreamWaitEvent(s, m->ev_lora, 0));
-    const int tensor_of[4] = {PB_T_WQ, PB_T_WK, PB_T_WV, PB_T_WO};
     for (int l = 0; l < c.n_layers; ++l) {
         if (int rc = wait_recorded(m, l)) return rc;
         HIP_TRY(hipStreamWaitEvent(s, m->ev_layer[l], 0));
+    }
+    if (c.merge_shadow) {
+        if (m->merged_slot >= 0) {  // switch: back to the unmerged weights first
+            if (int rc = copy_shadow(m, false)) return rc;
+        } else if (!m->shadow_valid) {
+            if (int rc = copy_shadow(m, true)) return rc;
+            m->shadow_valid = true;
+        }
+    }
+    m->merged_slot = -1;
+    m->dec_B = 0;  // a KV cache from before the merge belongs to another model
+    const int tensor_of[4] = {PB_T_WQ, PB_T_WK, PB_T_WV, PB_T_WO};
+    for (int l = 0; l < c.n_layers; ++l) {
         for (int t = 0; t < 4; ++t) {
             if (!((m->slot_mask[slot] >> t) & 1u)) continue;
             const char* At = m->at(a.loraA) + (size_t)l * a.loraA_layer + (size_t)t * a.kw * c.d_model * 2;
@@ -1173,7 +1222,17 @@ extern "C" int pb_merge_lora(pb_model* m, int32_t slot) {
     }
     HIP_TRY(hipStreamSynchronize(s));
     m->merged_slot = slot;
-    m->dec_B = 0;  // a KV cache from before the merge belongs to another model
+    return PB_OK;
+}
+
+extern "C" int pb_unmerge_lora(pb_model* m) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    if (!m->cfg.merge_shadow) return fail(PB_ESTATE, "the model keeps no merge shadow");
+    if (m->merged_slot < 0) return fail(PB_ESTATE, "no adapter is merged");
+    if (int rc = copy_shadow(m, false)) return rc;
+    HIP_TRY(hipStreamSynchronize(m->compute));
+    m->merged_slot = -1;
+    m->dec_B = 0;
     return PB_OK;
 }
 
