@@ -328,7 +328,7 @@ def main():
     flops = w.prefill_flops()["total"]
     tflops = flops / (ms_step / 1e3) / 1e12
 
-    # ---- per-kernel durations: same steps with HIP events around each launch --
+    # ---- per-kernel durations: same steps, events from the kernels' dispatch packets --
     m.reset_timing()
     m.set_timing(True)
     for _ in range(args.steps):
