@@ -18,7 +18,11 @@
 // 8 scores it already holds.  The V^T operand is read from the row-major V
 // tile with transposing LDS reads (ds_read_b64_tr_b16) in the same key order.
 //
-// Blocks run heaviest-first (the last query block sees the most keys).
+// Blocks run heaviest-first (the last query block sees the most keys).  When
+// query blocks are few (a short prompt), KS = 2 wave groups of 4 share a
+// block's queries and take alternating key tiles; the two online-softmax
+// states are merged through LDS at the end, halving the longest block's key
+// loop and putting two waves on each SIMD.
 #include "common.h"
 #include "kernels.h"
 
@@ -28,6 +32,9 @@ namespace {
 
 #ifndef PB_ATTN_QW32
 #define PB_ATTN_QW32 1  // allow 32 queries per wave
+#endif
+#ifndef PB_ATTN_KS2
+#define PB_ATTN_KS2 1  // allow two wave groups splitting the keys
 #endif
 
 constexpr float LOG2E = 1.4426950408889634f;
@@ -58,21 +65,24 @@ __device__ __forceinline__ u32x2 read_tr16(const uint8_t* p) {
     return __builtin_bit_cast(u32x2, v);
 }
 
-template <typename T, int HD, int QW>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(QW == 32 ? 2 : 1)))
+template <typename T, int HD, int QW, int KS>
+__global__ __launch_bounds__(256 * KS) __attribute__((amdgpu_waves_per_eu(QW == 32 || KS == 2 ? 2 : 1)))
 void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, int64_t kv_ld, int64_t kv_seq,
                       T* __restrict__ out, int T_len, int H) {
     typedef typename Mfma<T>::vec8 vec8;
-    constexpr int BQ = 4 * QW;         // queries per block (4 waves)
+    constexpr int NW = 4 * KS;         // waves per block
+    constexpr int BQ = 4 * QW;         // queries per block (4 waves per group)
     constexpr int NQG = QW / 16;       // 16-query groups per wave
     constexpr int CS = HD / 32;        // 32-wide k steps over head_dim
     constexpr int CT = HD / 16;        // 16-row tiles of O^T
     constexpr int RB = HD * 2;         // bytes per K/V row
     constexpr int CPR = RB / 16;       // 16-byte chunks per row
     constexpr int TILE = BKV * RB;     // bytes per K or V tile
-    constexpr int STAGE = 2 * TILE;    // K then V
-    constexpr int NI = STAGE / 1024;   // 1 KB DMA instructions per stage
-    constexpr int NL = NI / 4;         // ... per wave
+    constexpr int GSTAGE = 2 * TILE;   // one key tile: K then V
+    constexpr int STAGE = KS * GSTAGE; // one key tile per wave group
+    constexpr int NIG = GSTAGE / 1024; // 1 KB DMA instructions per key tile
+    constexpr int NI = STAGE / 1024;   // ... per stage
+    constexpr int NL = NI / NW;        // ... per wave
     constexpr int RPI = 1024 / RB;     // rows per DMA instruction
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
@@ -82,12 +92,13 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
     const int qb = nqb - 1 - (int)blockIdx.x;  // heaviest blocks first
     const int h = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int grp = wave / 4, wq = wave % 4;  // key-tile group, wave within it
     const int lr = lane & 15, lg = lane >> 4;
     const int64_t row0 = (int64_t)b * T_len;
     const T* Qb = qkv + h * HD;
 
     // Q^T operands stay in registers: query = q0 + 16 qg + lr
-    const int q0 = qb * BQ + wave * QW;
+    const int q0 = qb * BQ + wq * QW;
     vec8 qf[NQG][CS];
 #pragma unroll
     for (int qg = 0; qg < NQG; ++qg) {
@@ -97,17 +108,20 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
             qf[qg][cs] = as_vec8<T>(*(const u32x4*)(Qb + (row0 + qr) * ld + cs * 32 + 8 * lg));
     }
 
-    // DMA slot j of this wave: instruction I = wave + 4 j of the stage (K tile
-    // first, then V); lane i fills row RPI * (I % (NI / 2)) + i / CPR, physical
-    // chunk i % CPR, i.e. logical chunk (i % CPR) ^ permutation of that row.
+    // DMA slot j of this wave: instruction I = wave + NW j of the stage,
+    // key tile group I / NIG (tile KS it + group of iteration it), in it K
+    // then V; lane i fills row RPI * (I' % (NIG / 2)) + i / CPR (I' = I % NIG),
+    // physical chunk i % CPR, i.e. logical chunk (i % CPR) ^ permutation of
+    // that row.  Tiles past the last one re-read its key rows (not used).
     const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
-    auto issue = [&](int kb, int stage) {
+    auto issue = [&](int it, int stage) {
         const uint32_t sbase = lds0 + stage * STAGE;
 #pragma unroll
         for (int j = 0; j < NL; ++j) {
-            const int I = wave + 4 * j;
-            const bool isv = I >= NI / 2;
-            const int row = RPI * (I % (NI / 2)) + lane / CPR;
+            const int I = wave + NW * j;
+            const int kb = it * KS + I / NIG, Ig = I % NIG;
+            const bool isv = Ig >= NIG / 2;
+            const int row = RPI * (Ig % (NIG / 2)) + lane / CPR;
             const int pch = lane % CPR;
             const int ch = isv ? vswz<HD>(row, pch) : kswz(row, pch);
             const int key = min(kb * BKV + row, T_len - 1);
@@ -128,12 +142,15 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
 
     // keys needed by this block: those <= its last query (and < T)
     const int nkb = min((T_len + BKV - 1) / BKV, ((qb + 1) * BQ + BKV - 1) / BKV);
+    const int nit = (nkb + KS - 1) / KS;
     issue(0, 0);
-    for (int kb = 0; kb < nkb; ++kb) {
+    for (int it = 0; it < nit; ++it) {
         wait_vmcnt<0>();
-        __syncthreads();  // tile kb visible; stage of tile kb-1 free
-        if (kb + 1 < nkb) issue(kb + 1, (kb + 1) & 1);
-        const uint8_t* sK = smem + (kb & 1) * STAGE;
+        __syncthreads();  // tiles of iteration it visible; stage of it-1 free
+        if (it + 1 < nit) issue(it + 1, (it + 1) & 1);
+        const int kb = it * KS + grp;
+        if (kb >= nkb) continue;  // wave-uniform: this group has no tile left
+        const uint8_t* sK = smem + (it & 1) * STAGE + grp * GSTAGE;
         const uint8_t* sV = sK + TILE;
 
         // S^T tiles: key = kb*64 + 16 jt + 4 lg + r, query = q0 + 16 qg + lr
@@ -245,6 +262,40 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
         }
     }
 
+    if (KS == 2) {
+        // merge group 1's (max, sum, O^T) into group 0's: every lane holds
+        // the same query and O^T rows in both groups
+        float* xo = (float*)smem;                           // [4 waves][NQG][CT][64 lanes][4]
+        float* xm = xo + 4 * NQG * CT * 64 * 4;             // [4 waves][NQG][64 lanes][2]
+        __syncthreads();  // every wave is done with the ring
+        if (grp == 1) {
+#pragma unroll
+            for (int qg = 0; qg < NQG; ++qg) {
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct)
+                    *(f32x4*)(xo + (((wq * NQG + qg) * CT + ct) * 64 + lane) * 4) = o[qg][ct];
+                xm[((wq * NQG + qg) * 64 + lane) * 2] = m_run[qg];
+                xm[((wq * NQG + qg) * 64 + lane) * 2 + 1] = l_run[qg];
+            }
+        }
+        __syncthreads();
+        if (grp == 1) return;
+#pragma unroll
+        for (int qg = 0; qg < NQG; ++qg) {
+            const float m1 = xm[((wq * NQG + qg) * 64 + lane) * 2];
+            const float l1 = xm[((wq * NQG + qg) * 64 + lane) * 2 + 1];
+            const float M = fmaxf(m_run[qg], m1);  // finite: group 0 always sees key 0
+            const float a0 = __builtin_amdgcn_exp2f((m_run[qg] - M) * LOG2E);
+            const float a1 = __builtin_amdgcn_exp2f((m1 - M) * LOG2E);  // 0 when group 1 had no tile
+            l_run[qg] = l_run[qg] * a0 + l1 * a1;
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                const f32x4 o1 = *(const f32x4*)(xo + (((wq * NQG + qg) * CT + ct) * 64 + lane) * 4);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) o[qg][ct][r] = o[qg][ct][r] * a0 + o1[r] * a1;
+            }
+        }
+    }
 #pragma unroll
     for (int qg = 0; qg < NQG; ++qg) {
         const int q_idx = q0 + 16 * qg + lr;
@@ -260,30 +311,36 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
     }
 }
 
-template <typename T, int HD, int QW>
+template <typename T, int HD, int QW, int KS>
 hipError_t launch_hd(const void* qkv, const void* kv, int64_t kv_ld, int64_t kv_seq, void* out, int B,
                      int T_len, int H, hipStream_t s) {
-    constexpr int LDS = 2 * 2 * BKV * HD * 2;
+    constexpr int LDS = 2 * KS * 2 * BKV * HD * 2;  // two stages of KS key tiles (K and V)
+    static_assert(KS == 1 || 4 * QW / 16 * (HD / 16) * 64 * 16 + 4 * QW / 16 * 64 * 8 <= LDS,
+                  "the merge fits in the ring");
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void*)attention_kernel<T, HD, QW>,
+        hipError_t e = hipFuncSetAttribute((const void*)attention_kernel<T, HD, QW, KS>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     dim3 grid((T_len + 4 * QW - 1) / (4 * QW), H, B);
-    PB_LAUNCH((attention_kernel<T, HD, QW>), grid, dim3(256), LDS, s, (const T*)qkv, (const T*)kv,
-                       kv_ld, kv_seq, (T*)out, T_len, H);
+    PB_LAUNCH((attention_kernel<T, HD, QW, KS>), grid, dim3(256 * KS), LDS, s, (const T*)qkv, (const T*)kv,
+              kv_ld, kv_seq, (T*)out, T_len, H);
     return hipGetLastError();
 }
 
 template <typename T, int HD>
 hipError_t launch_qw(const void* qkv, const void* kv, int64_t kv_ld, int64_t kv_seq, void* out, int B,
                      int T_len, int H, hipStream_t s) {
-    // 32 queries per wave when 128-query blocks still give every CU work
+    // 32 queries per wave when 128-query blocks still give every CU work;
+    // with fewer than 512 blocks of 64 queries, two wave groups split the keys
     const long blocks128 = (long)((T_len + 127) / 128) * H * B;
-    if (PB_ATTN_QW32 && blocks128 >= 512) return launch_hd<T, HD, 32>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
-    return launch_hd<T, HD, 16>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
+    const long blocks64 = (long)((T_len + 63) / 64) * H * B;
+    if (PB_ATTN_QW32 && blocks128 >= 512) return launch_hd<T, HD, 32, 1>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
+    if (PB_ATTN_KS2 && blocks64 < 512 && T_len > BKV)
+        return launch_hd<T, HD, 16, 2>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
+    return launch_hd<T, HD, 16, 1>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
 }
 
 // ---- decode: one new query per (sequence, head) against the KV cache --------
