@@ -57,6 +57,12 @@ namespace {
 #ifndef PB_GEMM_GEMV
 #define PB_GEMM_GEMV 1  // weight-streaming kernel for at most 8 token rows
 #endif
+#ifndef PB_GEMV_KW8
+#define PB_GEMV_KW8 1  // GEMV rows of K >= 4096 split over eight waves
+#endif
+#ifndef PB_GEMV_RPB
+#define PB_GEMV_RPB 4  // output features per GEMV block
+#endif
 #ifndef PB_GEMM_S256
 #define PB_GEMM_S256 2  // ... of the 256 x 256 tiles
 #endif
@@ -514,25 +520,26 @@ hipError_t launch_typed(int role, const GemmParams& p, const GemmWorkspace& wsp,
 
 // ---- few rows (decode steps): weight streaming without tiles ---------------
 // A block owns four consecutive output features n0..n0+3; its four waves
-// split K (and the LoRA K2 columns) into four equal contiguous parts, so a
-// matrix of N features is streamed by N / 4 blocks and every CU has many
-// waves' loads in flight.  In a part, lane i takes elements 8i..8i+7 of each
+// (eight for rows of 4096 or more) split K (and the LoRA K2 columns) into
+// equal contiguous parts, so a matrix of N features is streamed by N / 4
+// blocks and every CU has many waves' loads in flight (measured: four
+// features per block beat eight or sixteen).  In a part, lane i takes elements 8i..8i+7 of each
 // 512-element chunk (a feature's chunk is one contiguous 1 KiB read), two
 // chunks per step, accumulating all MR token rows at once (MR <= GEMV_MAX_ROWS: the rows
 // of X are re-read from cache by every wave).  Each wave sums its lanes, the
-// four parts are added in wave order through LDS, and the usual epilogue is
+// parts are added in wave order through LDS, and the usual epilogue is
 // applied to the four features of each token.
-template <typename T, int MR>
+template <typename T, int MR, int RPB>
 __device__ __forceinline__ void gemv_dot(const T* __restrict__ X, int64_t ldx, const T* __restrict__ W,
                                          int64_t ldw, int n0, int M, int kb, int ke, int lane,
-                                         float (&acc)[4][MR]) {
+                                         float (&acc)[RPB][MR]) {
     for (int c0 = kb + lane * 8; c0 < ke; c0 += 2 * 512) {
-        u32x4 wr[2][4], xr[2][MR];
+        u32x4 wr[2][RPB], xr[2][MR];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
             const int c = min(c0 + u * 512, ke - 8);  // in bounds; the excess is not accumulated
 #pragma unroll
-            for (int r = 0; r < 4; ++r) wr[u][r] = *(const u32x4*)(W + (int64_t)(n0 + r) * ldw + c);
+            for (int r = 0; r < RPB; ++r) wr[u][r] = *(const u32x4*)(W + (int64_t)(n0 + r) * ldw + c);
 #pragma unroll
             for (int m = 0; m < MR; ++m) xr[u][m] = *(const u32x4*)(X + (int64_t)min(m, M - 1) * ldx + c);
         }
@@ -544,7 +551,7 @@ __device__ __forceinline__ void gemv_dot(const T* __restrict__ X, int64_t ldx, c
                 T xe[8];
                 __builtin_memcpy(xe, &xr[u][m], 16);
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
+                for (int r = 0; r < RPB; ++r) {
                     T we[8];
                     __builtin_memcpy(we, &wr[u][r], 16);
 #pragma unroll
@@ -555,52 +562,70 @@ __device__ __forceinline__ void gemv_dot(const T* __restrict__ X, int64_t ldx, c
     }
 }
 
-template <typename T, int EPI, int MR>
-__global__ __launch_bounds__(256) void gemv_kernel(GemmParams p) {
-    __shared__ float part[4][4][MR];  // [wave][feature][token]
+// RPB output features per block (a multiple of 4: the epilogue writes four
+// consecutive features of one token), K split over KW waves
+template <typename T, int EPI, int MR, int RPB, int KW>
+__global__ __launch_bounds__(64 * KW) void gemv_kernel(GemmParams p) {
+    __shared__ float part[KW][RPB][MR];  // [wave][feature][token]
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int n0 = blockIdx.x * 4;
-    float acc[4][MR];
+    const int n0 = blockIdx.x * RPB;
+    float acc[RPB][MR];
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+    for (int r = 0; r < RPB; ++r)
 #pragma unroll
         for (int m = 0; m < MR; ++m) acc[r][m] = 0.f;
-    const int q1 = p.K1 / 4;  // K1, K2 are multiples of 64: the parts are multiples of 16
-    gemv_dot<T, MR>((const T*)p.X, p.ldx, (const T*)p.W, p.ldw, n0, p.M, wave * q1, (wave + 1) * q1, lane, acc);
+    const int q1 = p.K1 / KW;  // K1, K2 are multiples of 64: the parts are multiples of 8
+    gemv_dot<T, MR, RPB>((const T*)p.X, p.ldx, (const T*)p.W, p.ldw, n0, p.M, wave * q1, (wave + 1) * q1, lane,
+                         acc);
     if (p.K2 > 0) {
-        const int g = n0 / p.group;
-        const int q2 = p.K2 / 4;
+        const int g = n0 / p.group;  // the group size is a multiple of RPB
+        const int q2 = p.K2 / KW;
         if ((p.k2_mask >> g) & 1u)
-            gemv_dot<T, MR>((const T*)p.X2 + (int64_t)g * p.x2_group_stride, p.ldx2, (const T*)p.W2, p.ldw2, n0,
-                            p.M, wave * q2, (wave + 1) * q2, lane, acc);
+            gemv_dot<T, MR, RPB>((const T*)p.X2 + (int64_t)g * p.x2_group_stride, p.ldx2, (const T*)p.W2, p.ldw2,
+                                 n0, p.M, wave * q2, (wave + 1) * q2, lane, acc);
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+    for (int r = 0; r < RPB; ++r)
 #pragma unroll
         for (int m = 0; m < MR; ++m) acc[r][m] = wave_sum(acc[r][m]);
     if (lane == 0)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
+        for (int r = 0; r < RPB; ++r)
 #pragma unroll
             for (int m = 0; m < MR; ++m) part[wave][r][m] = acc[r][m];
     __syncthreads();
-    const int m = threadIdx.x;
-    if (m < MR && m < p.M) {
+    const int m = threadIdx.x % MR, f4 = threadIdx.x / MR;  // token, group of four features
+    if (f4 < RPB / 4 && m < p.M) {
         f32x4 v;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = ((part[0][r][m] + part[1][r][m]) + part[2][r][m]) + part[3][r][m];
-        epilogue4<T, EPI>(p, m, n0, v);
+        for (int r = 0; r < 4; ++r) {
+            const int rr = 4 * f4 + r;
+            float t = part[0][rr][m];
+#pragma unroll
+            for (int w = 1; w < KW; ++w) t += part[w][rr][m];
+            v[r] = t;
+        }
+        epilogue4<T, EPI>(p, m, n0 + 4 * f4, v);
     }
 }
 
 template <typename T, int EPI>
 hipError_t launch_gemv(const GemmParams& p, hipStream_t s) {
-    const dim3 grid(p.N / 4);
-#define PB_GEMV(MR) PB_LAUNCH((gemv_kernel<T, EPI, MR>), grid, dim3(256), 0, s, p)
-    if (p.M <= 1) PB_GEMV(1);
-    else if (p.M <= 2) PB_GEMV(2);
-    else if (p.M <= 4) PB_GEMV(4);
-    else PB_GEMV(8);
+    constexpr int RPB = PB_GEMV_RPB;
+    const dim3 grid(p.N / RPB);
+#define PB_GEMV(MR, KW) PB_LAUNCH((gemv_kernel<T, EPI, MR, RPB, KW>), grid, dim3(64 * KW), 0, s, p)
+#define PB_GEMV_M(KW)                \
+    do {                             \
+        if (p.M <= 1) PB_GEMV(1, KW);      \
+        else if (p.M <= 2) PB_GEMV(2, KW); \
+        else if (p.M <= 4) PB_GEMV(4, KW); \
+        else PB_GEMV(8, KW);               \
+    } while (0)
+    // long rows: eight waves share the K range so each walks at most 1024
+    // elements (measured: eight waves for short rows of few blocks is slower)
+    if (PB_GEMV_KW8 && p.K1 >= 4096) PB_GEMV_M(8);
+    else PB_GEMV_M(4);
+#undef PB_GEMV_M
 #undef PB_GEMV
     return hipGetLastError();
 }

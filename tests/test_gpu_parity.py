@@ -29,6 +29,12 @@ SMALL = {
                           vocab=3000, max_pos=130, dtype="f16", batch=1, seq_len=130,
                           lora_targets=("q", "k", "v", "o"), lora_rank=32, lora_alpha=64.0,
                           n_adapters=1, layer_order=(2, 0, 1)),
+    # every adapter slot the library has (16), one per sequence, on all four
+    # projections: the packed LoRA width is 16 x 8 = 128 columns
+    "slots16": synth.Workload(name="slots16", seed=37, n_layers=2, d_model=256, n_heads=4, d_ffn=512,
+                              vocab=900, max_pos=32, dtype="bf16", batch=16, seq_len=20,
+                              lora_targets=("q", "k", "v", "o"), lora_rank=8, lora_alpha=16.0,
+                              n_adapters=16, adapter_of_seq=tuple(range(16))),
     # a single token per sequence and no adapters at all
     "one_token": synth.Workload(name="one_token", seed=34, n_layers=2, d_model=128, n_heads=2,
                                 d_ffn=256, vocab=500, max_pos=8, dtype="f16", batch=4, seq_len=1,
