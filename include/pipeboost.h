@@ -141,8 +141,10 @@ int pb_model_create(const pb_config* cfg, void* dev_arena, size_t arena_bytes, v
  * layer's last chunk.  host_layers[l] is layer l's blob (indexed by layer id,
  * not by position in the order); host_globals is the globals blob.  They stay
  * valid and unmodified until the next pb_prefill_first_token returns.
- * layer_order must be a permutation of 0..n_layers-1 and no blob NULL
- * (PB_EINVAL otherwise).  Blobs in pinned memory are copied by DMA from their
+ * layer_order lists n_layers distinct layer ids: all of them (a permutation
+ * of the model's layers) or, for a pipeline stage (pb_prefill_stage), a
+ * subset; a listed layer's blob must not be NULL (PB_EINVAL otherwise), and a
+ * prefill that needs an unlisted layer fails with PB_ESTATE.  Blobs in pinned memory are copied by DMA from their
  * own pages.  If any blob is pageable (hosts may cap locked memory below the
  * model's size), the library copies pageable blobs through its own pinned
  * staging ring (4 x 64 MiB, allocated on first use; PB_ENOMEM if it cannot
@@ -208,6 +210,24 @@ int pb_decode_step(pb_model* m, const int32_t* tokens, int32_t B, const int32_t*
  * at layer g * n_layers / n_gpus.  PB_EINVAL for bad sizes or no alive GPU. */
 int pb_plan_loading(int32_t n_layers, int32_t n_gpus, const uint8_t* alive, int32_t* order,
                     int32_t* block_first, int32_t* block_len);
+
+/* One pipeline stage of a prefill (Sections 4.2.1, 4.3.1: a GPU that holds a
+ * contiguous block of layers runs them and hands the hidden states on).
+ * Runs layers [layer_begin, layer_end) of B sequences of T tokens.  A stage
+ * starting at layer 0 embeds `tokens`; a later one reads the previous
+ * stage's hidden state from hidden_in (device, fp32 [B*T][d_model], row b*T+t).
+ * A stage ending before the last layer writes its hidden state to hidden_out
+ * (same layout; it may be the same buffer as hidden_in) and returns no
+ * tokens; the last stage returns the greedy tokens (and logits) like
+ * pb_prefill_first_token.  Only the stage's layers (and the globals) need to
+ * have been streamed: pb_stream_layers accepts a layer_order listing a subset
+ * of the layers.  Each layer waits for its own copy, as in a full prefill,
+ * and the results are bit-identical to one full prefill.  A stage leaves no
+ * decode state.  PB_EINVAL for a bad range or a missing buffer, PB_ESTATE
+ * when a needed layer was not streamed. */
+int pb_prefill_stage(pb_model* m, const int32_t* tokens, int32_t B, int32_t T, const int32_t* adapter_of_seq,
+                     int32_t layer_begin, int32_t layer_end, const float* hidden_in, float* hidden_out,
+                     int32_t* out_tokens, float* out_logits);
 
 /* Merged LoRA (Section 4.3.2): fold adapter slot `slot` into the device base
  * weights of every layer, W_t = dt(W_t + scale * B_t A_t) for each of its

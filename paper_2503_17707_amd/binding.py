@@ -77,6 +77,10 @@ _SIGS = {
                                      ctypes.POINTER(ctypes.c_float)]),
     "pb_invalidate_kv": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_uint8), ctypes.c_int32]),
     "pb_merge_lora": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32]),
+    "pb_prefill_stage": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
+                                        ctypes.c_int32, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
+                                        ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_float)]),
     "pb_unmerge_lora": (ctypes.c_int, [ctypes.c_void_p]),
     "pb_sched_create": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_void_p)]),
     "pb_sched_destroy": (ctypes.c_int, [ctypes.c_void_p]),
@@ -365,6 +369,28 @@ class Model:
             out_tok.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
             logits.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if want_logits else None))
         return out_tok, logits
+
+    def prefill_stage(self, tokens: np.ndarray, adapter_of_seq: Optional[Sequence[int]], layer_begin: int,
+                      layer_end: int, hidden_in=None, hidden_out=None, want_logits: bool = True):
+        """Layers [layer_begin, layer_end) of a prefill (pb_prefill_stage).  hidden_in /
+        hidden_out: device fp32 tensors of [B*T, d_model] (or None at the ends).
+        Returns (tokens, logits) from the last stage, None from the others."""
+        tokens = np.ascontiguousarray(tokens, dtype=np.int32)
+        B, T = tokens.shape
+        last = layer_end == self.cfg.n_layers
+        out_tok = np.empty(B, dtype=np.int32) if last else None
+        logits = np.empty((B, self.cfg.vocab), dtype=np.float32) if (last and want_logits) else None
+        ad = None
+        if adapter_of_seq is not None:
+            ad_arr = np.ascontiguousarray(adapter_of_seq, dtype=np.int32)
+            ad = ad_arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        check(lib().pb_prefill_stage(
+            self.h, tokens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), B, T, ad, layer_begin, layer_end,
+            ctypes.c_void_p(hidden_in.data_ptr()) if hidden_in is not None else None,
+            ctypes.c_void_p(hidden_out.data_ptr()) if hidden_out is not None else None,
+            out_tok.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)) if last else None,
+            logits.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if logits is not None else None))
+        return (out_tok, logits) if last else None
 
     def decode(self, tokens: np.ndarray, adapter_of_seq: Optional[Sequence[int]] = None,
                want_logits: bool = True):

@@ -591,20 +591,20 @@ int pb_stream_layers(pb_model* m, const int32_t* layer_order, int32_t n_layers,
     if (m->loader.joinable()) m->loader.join();
     m->load_rc = 0;
     const int L = m->cfg.n_layers;
-    if (n_layers != L) return fail(PB_EINVAL, "layer_order has %d entries, the model %d layers", n_layers, L);
+    if (n_layers < 1 || n_layers > L)
+        return fail(PB_EINVAL, "layer_order has %d entries, the model %d layers", n_layers, L);
     if (!layer_order || !host_layers || !host_globals) return fail(PB_EINVAL, "NULL argument");
     std::vector<char> seen(L, 0);
-    for (int i = 0; i < L; ++i) {
+    for (int i = 0; i < n_layers; ++i) {
         const int l = layer_order[i];
-        if (l < 0 || l >= L || seen[l]) return fail(PB_EINVAL, "layer_order is not a permutation of 0..%d", L - 1);
+        if (l < 0 || l >= L || seen[l]) return fail(PB_EINVAL, "layer_order entry %d is out of range or repeated", l);
         seen[l] = 1;
-    }
-    for (int l = 0; l < L; ++l)
         if (!host_layers[l]) return fail(PB_EINVAL, "layer %d blob is NULL", l);
+    }
     const size_t lb = m->lay.layer_bytes, gb = m->gl.total * 2;
     std::vector<LoadJob> jobs;
     jobs.push_back({(const char*)host_globals, m->at(m->lay.globals), gb, is_pinned(host_globals, gb), -1});
-    for (int i = 0; i < L; ++i) {
+    for (int i = 0; i < n_layers; ++i) {
         const int l = layer_order[i];
         jobs.push_back({(const char*)host_layers[l], m->layer_ptr(l), lb, is_pinned(host_layers[l], lb), l});
     }
@@ -624,7 +624,7 @@ int pb_stream_layers(pb_model* m, const int32_t* layer_order, int32_t n_layers,
         m->load_err.clear();
     }
     HIP_TRY(hipEventRecord(m->ev_load0, m->copy));
-    m->last_load_bytes = (double)gb + (double)L * (double)lb;
+    m->last_load_bytes = (double)gb + (double)n_layers * (double)lb;
     m->merged_slot = -1;  // the base weights arrive unmerged
     m->shadow_valid = false;
     if (all_pinned) {
@@ -778,8 +778,18 @@ struct Timed {
 // stream waits for each layer's copy event before the layer's first kernel
 // (the pipelined cold start); without, every weight must already be resident
 // (a recorded pass holds no waits on the load's events).
+// One pipeline stage's share of the forward pass: layers [l0, l1), the
+// hidden state (fp32 [N, d], device) taken from `in` unless the stage starts
+// at layer 0 (embedding) and handed to `out` unless it ends at the last layer
+// (final LayerNorm, LM head, argmax).
+struct Stage {
+    int l0, l1;
+    const float* in;
+    float* out;
+};
+
 int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_union, bool decode,
-                    const uint8_t* has_kv, bool wait_loads) {
+                    const uint8_t* has_kv, bool wait_loads, const Stage* st = nullptr) {
     const pb_config& c = m->cfg;
     const ArenaLayout& a = m->lay;
     const int dt = c.dtype;
@@ -804,12 +814,15 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
         return PB_OK;
     };
 
+    const int l0 = st ? st->l0 : 0, l1 = st ? st->l1 : L;
     if (int rc = wait_layer(-1)) return rc;
     if (use_lora && wait_loads) HIP_TRY(hipStreamWaitEvent(s, m->ev_lora, 0));
-    {
+    if (l0 == 0) {
         Timed t(m, PB_K_EMBED);
         HIP_TRY(pb::launch_embed(dt, (const int32_t*)m->at(a.tokens), m->gtensor(PB_G_EMBED),
                                  m->gtensor(PB_G_POS), x, N, T, d, pos0, s));
+    } else {  // the previous stage's hidden state
+        HIP_TRY(hipMemcpyAsync(x, st->in, (size_t)N * d * 4, hipMemcpyDeviceToDevice, s));
     }
     const bool qkv_lora = use_lora && (lora_union & (PB_LORA_Q | PB_LORA_K | PB_LORA_V));
     const bool o_lora = use_lora && (lora_union & PB_LORA_O);
@@ -828,7 +841,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
         return sh;
     };
     bool ln1_ready = false;  // LN1 (and its fused shrink) of layer l produced by layer l-1's fc2 reduce
-    for (int l = 0; l < L; ++l) {
+    for (int l = l0; l < l1; ++l) {
         if (int rc = wait_layer(l)) return rc;
         char* Aq = m->at(a.loraA) + (size_t)l * a.loraA_layer;  // [4][kw][d]
         char* Bq = m->at(a.loraB) + (size_t)l * a.loraB_layer;  // [4][d][kw]
@@ -926,7 +939,7 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             p.R = x; p.ldr = d;
             // the next layer's LN1 rides on the split-K reduce when the launcher
             // splits; its weights are read here, so wait for that layer first
-            if (l + 1 < L) {
+            if (l + 1 < l1) {
                 if (int rc = wait_layer(l + 1)) return rc;
                 p.ln_g = m->ltensor(l + 1, PB_T_LN1_G); p.ln_b = m->ltensor(l + 1, PB_T_LN1_B);
                 p.ln_out = u; p.ln_eps = c.ln_eps; p.ln_done = &ln1_ready;
@@ -934,6 +947,10 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
             }
             HIP_TRY(pb::launch_gemm(dt, 3, pb::EPI_RESID, p, gws, s));
         }
+    }
+    if (l1 < L) {  // hand the hidden state to the next stage
+        HIP_TRY(hipMemcpyAsync(st->out, x, (size_t)N * d * 4, hipMemcpyDeviceToDevice, s));
+        return PB_OK;
     }
     float* zf = (float*)m->at(a.zf);
     {
@@ -1018,7 +1035,7 @@ int forward_graph(pb_model* m, int B, int T, bool use_lora, uint32_t lora_union,
 // greedy tokens (and logits) of B sequences of T new tokens at position pos0.
 static int run_forward(pb_model* m, const int32_t* tokens, int32_t B, int32_t T,
                        const int32_t* adapter_of_seq, int32_t* out_tokens, float* out_logits, int pos0,
-                       bool decode, const uint8_t* has_kv = nullptr) {
+                       bool decode, const uint8_t* has_kv = nullptr, const Stage* st = nullptr) {
     const pb_config& c = m->cfg;
     const int N = B * T;
     for (int i = 0; i < N; ++i)
@@ -1048,19 +1065,25 @@ static int run_forward(pb_model* m, const int32_t* tokens, int32_t B, int32_t T,
     HIP_TRY(hipMemcpyAsync(m->at(a.rowslot), m->h_rowslot, (size_t)N * 4, hipMemcpyHostToDevice, s));
     HIP_TRY(hipMemcpyAsync(m->at(a.slotscale), m->h_scale, SMALL_WORDS * 4, hipMemcpyHostToDevice, s));
     int rc = 1;
-    if (m->graphs_on && !m->timing && !has_kv && weights_settled(m, use_lora))
+    if (m->graphs_on && !m->timing && !has_kv && !st && weights_settled(m, use_lora))
         rc = forward_graph(m, B, T, use_lora, lora_union, decode);
-    if (rc == 1) rc = enqueue_forward(m, B, T, use_lora, lora_union, decode, has_kv, true);
+    if (rc == 1) rc = enqueue_forward(m, B, T, use_lora, lora_union, decode, has_kv, true, st);
     if (rc) {
         (void)hipStreamSynchronize(s);
         return rc;
     }
-    HIP_TRY(hipMemcpyAsync(m->h_outtok, m->at(a.outtok), (size_t)B * 4, hipMemcpyDeviceToHost, s));
-    if (out_logits)
-        HIP_TRY(hipMemcpyAsync(m->h_logits, m->at(a.logits), (size_t)B * c.vocab * 4, hipMemcpyDeviceToHost, s));
+    const bool head = !st || st->l1 == c.n_layers;  // this call ends with the first tokens
+    if (head) {
+        HIP_TRY(hipMemcpyAsync(m->h_outtok, m->at(a.outtok), (size_t)B * 4, hipMemcpyDeviceToHost, s));
+        if (out_logits)
+            HIP_TRY(hipMemcpyAsync(m->h_logits, m->at(a.logits), (size_t)B * c.vocab * 4, hipMemcpyDeviceToHost,
+                                   s));
+    }
     HIP_TRY(hipStreamSynchronize(s));
-    std::memcpy(out_tokens, m->h_outtok, (size_t)B * 4);
-    if (out_logits) std::memcpy(out_logits, m->h_logits, (size_t)B * c.vocab * 4);
+    if (head) {
+        std::memcpy(out_tokens, m->h_outtok, (size_t)B * 4);
+        if (out_logits) std::memcpy(out_logits, m->h_logits, (size_t)B * c.vocab * 4);
+    }
     if (m->timing) {
         for (size_t i = 0; i + 1 < m->tused; i += 2) {
             float ms = 0.f;
@@ -1094,6 +1117,27 @@ extern "C" int pb_prefill_first_token(pb_model* m, const int32_t* tokens, int32_
         for (int b = 0; b < B; ++b) m->dec_adapter[b] = adapter_of_seq ? adapter_of_seq[b] : -1;
     }
     return PB_OK;
+}
+
+extern "C" int pb_prefill_stage(pb_model* m, const int32_t* tokens, int32_t B, int32_t T,
+                                const int32_t* adapter_of_seq, int32_t layer_begin, int32_t layer_end,
+                                const float* hidden_in, float* hidden_out, int32_t* out_tokens, float* out_logits) {
+    if (!m) return fail(PB_EINVAL, "model is NULL");
+    const pb_config& c = m->cfg;
+    const int L = c.n_layers;
+    if (!tokens) return fail(PB_EINVAL, "tokens must be non-NULL");
+    if (B < 1 || B > c.max_batch) return fail(PB_EINVAL, "B=%d outside [1, %d]", B, c.max_batch);
+    if (T < 1 || T > c.max_pos) return fail(PB_EINVAL, "T=%d outside [1, %d]", T, c.max_pos);
+    if ((int64_t)B * T > c.max_tokens) return fail(PB_EINVAL, "B*T=%lld exceeds max_tokens=%d", (long long)B * T, c.max_tokens);
+    if (layer_begin < 0 || layer_end <= layer_begin || layer_end > L)
+        return fail(PB_EINVAL, "layers [%d, %d) are not a range of 0..%d", layer_begin, layer_end, L);
+    if (layer_begin > 0 && !hidden_in) return fail(PB_EINVAL, "a stage after layer 0 needs hidden_in");
+    if (layer_end < L && !hidden_out) return fail(PB_EINVAL, "a stage before the last layer needs hidden_out");
+    if (layer_end == L && !out_tokens) return fail(PB_EINVAL, "the last stage needs out_tokens");
+    if (!m->streamed) return fail(PB_ESTATE, "prefill before pb_stream_layers");
+    m->dec_B = 0;  // a stage leaves nothing to decode from
+    const Stage st{layer_begin, layer_end, hidden_in, hidden_out};
+    return run_forward(m, tokens, B, T, adapter_of_seq, out_tokens, out_logits, 0, false, nullptr, &st);
 }
 
 extern "C" int pb_decode_step(pb_model* m, const int32_t* tokens, int32_t B, const int32_t* adapter_of_seq,

@@ -27,8 +27,8 @@ def test_error_codes():
         with pytest.raises(pb.PbError) as e:
             m.prefill(toks)
         assert e.value.code == pb.PB_ESTATE
-        # not a permutation
-        for bad in ([0, 0], [1, 2], [0]):
+        # repeated, out of range, empty or too many layer ids
+        for bad in ([0, 0], [1, 2], [], [0, 1, 0]):
             arr = (ctypes.c_int32 * len(bad))(*bad)
             ptrs = (ctypes.c_void_p * 2)(*[b.ptr for b in hw.layers])
             rc = L.pb_stream_layers(m.h, arr, len(bad), ptrs, ctypes.c_void_p(hw.globals.ptr))
@@ -38,6 +38,12 @@ def test_error_codes():
         arr = (ctypes.c_int32 * 2)(0, 1)
         ptrs = (ctypes.c_void_p * 2)(None, hw.layers[1].ptr)
         assert L.pb_stream_layers(m.h, arr, 2, ptrs, ctypes.c_void_p(hw.globals.ptr)) == pb.PB_EINVAL
+        # a subset of the layers (a pipeline stage's share) streams, but a full
+        # prefill needs the layer it lacks
+        m.stream_layers(hw, [0])
+        with pytest.raises(pb.PbError) as e:
+            m.prefill(toks)
+        assert e.value.code == pb.PB_ESTATE
         # a valid stream, then argument errors of the prefill
         m.stream_layers(hw)
         with pytest.raises(pb.PbError) as e:
