@@ -85,7 +85,8 @@ def test_gemm_epilogues(kind, M, N, K, epi):
 
 @pytest.mark.parametrize("kind,hd,B,T,H", [("f16", 64, 2, 200, 3), ("bf16", 64, 1, 37, 2),
                                            ("f16", 128, 1, 130, 2), ("bf16", 128, 2, 64, 1),
-                                           ("f16", 128, 1, 1100, 4), ("f16", 64, 1, 1, 2)])
+                                           ("f16", 128, 1, 1100, 4), ("f16", 64, 1, 1, 2),
+                                           ("bf16", 64, 1, 530, 2), ("f16", 64, 2, 129, 2)])
 def test_attention(kind, hd, B, T, H):
     import torch
 
