@@ -18,6 +18,11 @@ B=1, T=512, LoRA rank 16 on q and v, fp16 weights, random init) is synthetic.
   weight bytes read per second against HBM), checked against the oracle's
   stored decode logits when present.
 * cpu_baseline: the CPU oracle timed on a bounded sample of the same workload.
+
+Separate modes (each prints its own JSON line and exits): --h2d-sweep (pinned
+copy rates), --calibrate-copy-mib (the reference copy for HBM byte counters),
+--gemm-reference (the projection GEMMs through these kernels and through the
+vendor library on the same operands, as a reference point).
 """
 import argparse
 import gc
@@ -199,6 +204,56 @@ def h2d_sweep(w, pb, torch, np):
                           "best_frac_of_pcie": best / PCIE5_X16_GBPS}}
 
 
+def gemm_reference(w, pb, torch, reps=40):
+    """The workload's four projection GEMMs (no LoRA tiles) through this
+    library's kernels (pb_op_gemm: the model's tile plan and epilogues; o and
+    fc2 with their plain split-K reduce, without the LayerNorm the model fuses
+    into it) and through the vendor library behind torch's linear (bias
+    added), on the same device operands: events around `reps` back-to-back
+    launches, after a warm-up.  A reference point for the kernels' rate, not
+    part of the path."""
+    d, f, n = w.d_model, w.d_ffn, w.batch * w.seq_len
+    dt = torch.float16 if w.dtype == "f16" else torch.bfloat16
+    dcode = 1 if w.dtype == "f16" else 0
+    ws_bytes = max(64 << 20, min(1 << 30, 4 * n * d * 4))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda:0")
+    g = torch.Generator(device="cuda:0").manual_seed(5)
+    shapes = [("qkv", 3 * d, d, 0), ("o", d, d, 2), ("fc1", f, d, 1), ("fc2", d, f, 2)]
+    out = {}
+    for name, N, K, epi in shapes:
+        X = torch.randn(n, K, device="cuda:0", generator=g).to(dt)
+        W = (torch.randn(N, K, device="cuda:0", generator=g) * 0.02).to(dt)
+        b = (torch.randn(N, device="cuda:0", generator=g) * 0.02).to(dt)
+        C = torch.empty(n, N, dtype=dt, device="cuda:0") if epi != 2 else None
+        R = torch.zeros(n, N, dtype=torch.float32, device="cuda:0") if epi == 2 else None
+
+        def ours():
+            pb.op_gemm(dcode, epi, X, W, b, C=C, R=R, qscale=d ** -0.5 if epi == 0 else 1.0,
+                       qcols=d if epi == 0 else 0, workspace=ws)
+
+        def library():
+            torch.nn.functional.linear(X, W, b)
+
+        row = {"M": n, "N": N, "K": K}
+        for label, fn in (("this_library", ours), ("vendor_library", library)):
+            for _ in range(5):
+                fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / reps
+            row[label] = {"us": us, "tflops": 2.0 * n * N * K / us / 1e6}
+        row["this_over_vendor_time"] = row["this_library"]["us"] / row["vendor_library"]["us"]
+        out[name] = row
+        del X, W, b, C, R
+    return {"gemm_reference": {"workload": w.name, "dtype": w.dtype, "launches_timed": reps,
+                               "shapes": out}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -214,6 +269,9 @@ def main():
                          "the reference kernel for scaling HBM byte counters")
     ap.add_argument("--decode-steps", type=int, default=32,
                     help="greedy decode steps timed after the prefill (0 = none)")
+    ap.add_argument("--gemm-reference", action="store_true",
+                    help="only time the workload's four projection GEMMs through this library's "
+                         "kernels and through the vendor library (torch's linear), then exit")
     ap.add_argument("--h2d-sweep", action="store_true",
                     help="only measure the loader's H2D rate over chunk sizes, and plain pinned "
                          "copies on one and two streams, then exit")
@@ -244,6 +302,9 @@ def main():
     w = synth.WORKLOADS[args.workload]
     if args.h2d_sweep:
         print(json.dumps(h2d_sweep(w, pb, torch, np)), flush=True)
+        return
+    if args.gemm_reference:
+        print(json.dumps(gemm_reference(w, pb, torch)), flush=True)
         return
     dev = torch.device("cuda:0")
     t0 = time.perf_counter()
