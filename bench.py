@@ -505,6 +505,9 @@ def main():
                        "h2d_GBps_during_cold_start": float(np.median(loads)),
                        "h2d_GBps_alone": b_meas, "pcie_gen5_x16_GBps": PCIE5_X16_GBPS,
                        "bound_ms": bound_ms, "frac_of_bound": bound_ms / ttft_med,
+                       # the same bytes at the link rate (32 GT/s x 16 lanes, 128b/130b)
+                       "link_bound_ms": total_h2d / (PCIE5_X16_GBPS * 1e6),
+                       "frac_of_link_bound": total_h2d / (PCIE5_X16_GBPS * 1e6) / ttft_med,
                        "bound_terms_ms": {"h2d_bytes_over_B_meas": bound_ms,
                                           "flops_over_warm_rate": ms_step},
                        "ttft_over_max_bound": ttft_med / max(bound_ms, ms_step),
