@@ -30,6 +30,16 @@
       that kind's launches.  Ends with the block bench.py reads (bytes per
       launch, valid while the kernel sources keep the printed hash).
 
+  python -m paper_2503_17707_amd.profsum stalls DIR_A DIR_B LABEL
+      DIR_A from `rocprofv3 --pmc SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_ANY
+      SQ_WAIT_INST_ANY SQ_ACTIVE_INST_ANY SQ_VALU_MFMA_BUSY_CYCLES SQ_ACTIVE_INST_LDS
+      SQ_ACTIVE_INST_VMEM GRBM_GUI_ACTIVE -f csv -d DIR_A -o c -- python bench.py
+      --workload W --gemm-reference`, DIR_B the same with SQ_WAIT_INST_LDS
+      SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE SQ_LDS_DATA_FIFO_FULL SQ_LDS_CMD_FIFO_FULL
+      SQ_ACTIVE_INST_VALU SQ_ACTIVE_INST_SCA SQ_INSTS_LDS GRBM_GUI_ACTIVE: where the
+      GEMM waves' cycles go, for this library's GEMM kernels (by tile and role)
+      and the vendor library's, side by side.
+
 Only reads files; used to write the summaries kept with the profiles.
 """
 import collections
@@ -243,8 +253,53 @@ def traffic(fetch, write, cal_fetch, cal_write, label):
     return "\n".join(out)
 
 
+def _gemm_key(name):
+    m = re.search(r"gemm_kernelIDF16b?_((?:Li\d+E)+)", name)
+    if m:
+        a = [int(x) for x in re.findall(r"Li(\d+)E", m.group(1))]
+        return "this library %dx%d, %d waves, %s" % (a[1], a[2], 64 * a[3] * a[4] // 64,
+                                                    {0: "qkv", 1: "o", 2: "fc1", 3: "o/fc2"}.get(a[5], "?"))
+    m = re.search(r"(MT\d+x\d+x\d+)", name)
+    if "Cijk" in name and m:
+        return "vendor library " + m.group(1)
+    return None
+
+
+def stalls(dir_a, dir_b, label):
+    per = collections.defaultdict(lambda: collections.defaultdict(list))
+    for d in (dir_a, dir_b):
+        for r in csv.DictReader(open(_one(d, "*counter_collection.csv"))):
+            k = _gemm_key(r["Kernel_Name"])
+            if k:
+                per[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    out = ["# Where the GEMM waves' cycles go, %s\n" % label,
+           "Kernel sources (paper_2503_17707_amd/csrc/*) sha256: `%s`\n" % source_sha256(),
+           "Counters per dispatch (dispatches serialized by the counter runs), averaged per kernel.  "
+           "Per wave-cycle: SQ_WAIT_ANY (waiting at a wait-count or barrier), SQ_WAIT_INST_ANY "
+           "(ready but waiting to issue), SQ_ACTIVE_INST_ANY / _LDS / _VMEM / _VALU, each over "
+           "SQ_WAVE_CYCLES.  MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 XCDs x 1024 "
+           "SIMDs); LDS active = SQ_LDS_IDX_ACTIVE / (GRBM_GUI_ACTIVE / 8), summed over the shader "
+           "engines; bank conflicts as a share of it.\n",
+           "| kernel | dispatches | MFMA busy | wait | wait to issue | active | LDS instr active | VMEM instr "
+           "active | VALU active | LDS active | LDS bank conflict share |",
+           "|---|---|---|---|---|---|---|---|---|---|---|"]
+    for k in sorted(per):
+        c = {n: sum(v) / len(v) for n, v in per[k].items()}
+        wc = c.get("SQ_WAVE_CYCLES", 0.0)
+        g = c.get("GRBM_GUI_ACTIVE", 0.0) / N_XCD
+        if not wc or not g:
+            continue
+        out.append("| %s | %d | %.3f | %.2f | %.2f | %.2f | %.2f | %.2f | %.2f | %.1f | %.2f |" % (
+            k, len(per[k].get("SQ_WAVE_CYCLES", [])), c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) / (g * N_SIMD),
+            c.get("SQ_WAIT_ANY", 0) / wc, c.get("SQ_WAIT_INST_ANY", 0) / wc, c.get("SQ_ACTIVE_INST_ANY", 0) / wc,
+            c.get("SQ_ACTIVE_INST_LDS", 0) / wc, c.get("SQ_ACTIVE_INST_VMEM", 0) / wc,
+            c.get("SQ_ACTIVE_INST_VALU", 0) / wc, c.get("SQ_LDS_IDX_ACTIVE", 0) / g,
+            c.get("SQ_LDS_BANK_CONFLICT", 0) / max(1.0, c.get("SQ_LDS_IDX_ACTIVE", 0))))
+    return "\n".join(out)
+
+
 def main(argv):
-    usage = {"overlap": (3, 4), "mfma": (3, 3), "kernels": (3, 3), "traffic": (6, 6)}
+    usage = {"overlap": (3, 4), "mfma": (3, 3), "kernels": (3, 3), "traffic": (6, 6), "stalls": (4, 4)}
     if not argv or argv[0] not in usage or not usage[argv[0]][0] <= len(argv) <= usage[argv[0]][1]:
         raise SystemExit(__doc__)
     if argv[0] == "overlap":
@@ -254,6 +309,8 @@ def main(argv):
         print(mfma(argv[1], argv[2]))
     elif argv[0] == "kernels":
         print(kernels(argv[1], argv[2]))
+    elif argv[0] == "stalls":
+        print(stalls(argv[1], argv[2], argv[3]))
     else:
         print(traffic(*argv[1:6]))
 
