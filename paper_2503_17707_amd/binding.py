@@ -279,8 +279,19 @@ class HostWeights:
         self.loras: Dict[int, List[Pinned]] = {}
 
     def _zero_padding(self, blob: Pinned, cfg: Config):
-        # every byte of the blob is written by a tensor except alignment gaps
-        ctypes.memset(blob.ptr, 0, blob.nbytes)
+        # every byte of the blob is written by a tensor except the alignment
+        # gaps between them: zero only those (the tensors' own fills touch the
+        # rest first, from all of the generator's threads)
+        import synth
+
+        spans = sorted(layer_tensor(cfg, n) for n in synth.LAYER_TENSORS)
+        pos = 0
+        for off, n in spans:
+            if 2 * off > pos:
+                ctypes.memset(blob.ptr + pos, 0, 2 * off - pos)
+            pos = max(pos, 2 * (off + n))
+        if blob.nbytes > pos:
+            ctypes.memset(blob.ptr + pos, 0, blob.nbytes - pos)
 
     def lora_mask(self) -> int:
         m = 0

@@ -9,7 +9,7 @@ def build(verbose: bool = False) -> str:
     src = os.path.join(HERE, "synth.c")
     out = os.path.join(HERE, "libsynth.so")
     tmp = out + ".tmp%d" % os.getpid()
-    cmd = ["gcc", "-O3", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off", "-std=c11",
+    cmd = ["gcc", "-O3", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off", "-mavx2", "-fno-math-errno", "-std=c11",
            "-Wall", "-o", tmp, src, "-lm"]
     if verbose:
         print(" ".join(cmd))

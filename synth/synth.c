@@ -160,36 +160,55 @@ static inline void box_muller(uint32_t xe, uint32_t xo, double* n0, double* n1) 
 double synth_ln_unit(double u) { return ln_unit(u); }
 void synth_cos_sin_turn(double f, double* c, double* s) { cos_sin_turn(f, c, s); }
 
-/* float -> IEEE binary16, round to nearest even (handles subnormals, inf, nan). */
-static inline uint16_t f32_to_f16_rne(float f) {
+/*
+ * float -> IEEE binary16, round to nearest even (subnormals, inf and nan
+ * included).  Every case is computed and the right one selected, so the
+ * conversion loop runs as vector code:
+ *   normal half (|x| >= 2^-14): exponent rebiased 127 -> 15, mantissa cut
+ *   to 10 bits, rounded on the 13 dropped bits (a carry may bump the
+ *   exponent, up to inf);
+ *   subnormal half (2^-25 <= |x| < 2^-14): the 24-bit significand shifted
+ *   right by 126 - e (14..24) in units of 2^-24, rounded on the dropped bits;
+ *   below 2^-25: zero; rounding to >= 65520: inf; nan stays a quiet nan.
+ */
+/* 0/1 comparisons and a select on 32-bit values below 2^31, in plain
+   arithmetic (no branches, no boolean vectors) */
+static inline uint32_t gt31(uint32_t a, uint32_t b) { return (b - a) >> 31; }
+static inline uint32_t eq31(uint32_t a, uint32_t b) { return ((a ^ b) - 1u) >> 31; }
+static inline uint32_t sel31(uint32_t c, uint32_t a, uint32_t b) {
+    uint32_t mask = 0u - c;
+    return (a & mask) | (b & ~mask);
+}
+
+static inline uint32_t f32_to_f16_bits32(float f) {
     uint32_t x;
     memcpy(&x, &f, 4);
     uint32_t sign = (x >> 16) & 0x8000u;
     uint32_t ax = x & 0x7FFFFFFFu;
-    if (ax >= 0x7F800000u) { /* inf or nan */
-        return (uint16_t)(sign | 0x7C00u | (ax > 0x7F800000u ? 0x200u : 0u));
-    }
-    if (ax >= 0x477FF000u) { /* rounds to >= 65520 -> inf */
-        return (uint16_t)(sign | 0x7C00u);
-    }
-    if (ax < 0x38800000u) { /* below the smallest normal half: 2^-14 */
-        if (ax < 0x33000000u) return (uint16_t)sign; /* < 2^-25 rounds to 0 */
-        uint32_t e = ax >> 23;
-        uint32_t m = (ax & 0x7FFFFFu) | 0x800000u;
-        uint32_t shift = 126u - e; /* 14..24: value = m * 2^(e-150), half subnormal unit 2^-24 */
-        uint32_t q = m >> shift;
-        uint32_t rem = m & ((1u << shift) - 1u);
-        uint32_t halfway = 1u << (shift - 1u);
-        if (rem > halfway || (rem == halfway && (q & 1u))) q += 1u;
-        return (uint16_t)(sign | q);
-    }
-    uint32_t e = (ax >> 23) - 112u; /* rebias 127 -> 15 */
+    uint32_t e = ax >> 23;
     uint32_t m = ax & 0x7FFFFFu;
-    uint32_t q = (e << 10) | (m >> 13);
-    uint32_t rem = m & 0x1FFFu;
-    if (rem > 0x1000u || (rem == 0x1000u && (q & 1u))) q += 1u; /* carry may bump exponent: fine */
-    return (uint16_t)(sign | q);
+    uint32_t qn = ((e - 112u) << 10) | (m >> 13);
+    uint32_t remn = m & 0x1FFFu;
+    qn += gt31(remn, 0x1000u) | (eq31(remn, 0x1000u) & qn & 1u);
+    /* subnormal shift 126 - e, used only for e in [102, 112]; e is clamped
+       there so that every shift is defined */
+    uint32_t ec = e < 102u ? 102u : e;
+    ec = ec > 112u ? 112u : ec;
+    uint32_t sh = 126u - ec;
+    uint32_t ms = m | 0x800000u;
+    uint32_t qs = ms >> sh;
+    uint32_t rems = ms & ((1u << sh) - 1u);
+    uint32_t half = 1u << (sh - 1u);
+    qs += gt31(rems, half) | (eq31(rems, half) & qs & 1u);
+    uint32_t r = qn;
+    r = sel31(gt31(0x38800000u, ax), qs, r);
+    r = sel31(gt31(0x33000000u, ax), 0u, r);
+    r = sel31(1u - gt31(0x477FF000u, ax), 0x7C00u, r);
+    r = sel31(1u - gt31(0x7F800000u, ax), 0x7C00u | (gt31(ax, 0x7F800000u) << 9), r);
+    return sign | r;
 }
+
+static inline uint16_t f32_to_f16_rne(float f) { return (uint16_t)f32_to_f16_bits32(f); }
 
 /* float -> bfloat16, round to nearest even. */
 static inline uint16_t f32_to_bf16_rne(float f) {
@@ -207,38 +226,166 @@ uint16_t synth_f32_to_bf16(float f) { return f32_to_bf16_rne(f); }
 enum { SYNTH_F32 = 0, SYNTH_F16 = 1, SYNTH_BF16 = 2 };
 
 /*
+ * Draws of NB consecutive Philox blocks (4 NB elements), computed stage by
+ * stage over arrays: Philox for every block, then ln and sqrt of every pair,
+ * then cos and sin, then the products.  Each stage is a loop without
+ * branches that the compiler turns into vector code, and every element goes
+ * through exactly the operations of philox_block, ln_unit and cos_sin_turn
+ * above, in the same order (selects replace their branches; the exponent is
+ * turned into a double by the exact 2^52 trick instead of an integer
+ * conversion), so the draws are bit for bit those of the scalar functions.
+ */
+#define NB 256
+
+static inline uint64_t dbits(double x) {
+    uint64_t b;
+    memcpy(&b, &x, 8);
+    return b;
+}
+
+static inline double bdbl(uint64_t b) {
+    double x;
+    memcpy(&x, &b, 8);
+    return x;
+}
+
+/* an integer 0 <= k < 2^52 as a double, exactly (2^52 + k has k in its mantissa) */
+static inline double small_int(uint64_t k) {
+    return bdbl(k | 0x4330000000000000ull) - 4503599627370496.0;
+}
+
+/* Box-Muller radius, cos and sin for NB word pairs (x_even, x_odd). */
+static inline void pair_stage(const uint32_t* restrict we, const uint32_t* restrict wo,
+                              double* restrict rad, double* restrict cs, double* restrict sn) {
+    for (int b = 0; b < NB; ++b) {
+        /* r = sqrt(-2 ln u1), ln as in ln_unit */
+        double u = (small_int(we[b]) + 0.5) * INV_2_32;
+        uint64_t bits = dbits(u);
+        /* m in [1, 2) from the mantissa; m > sqrt(2) compared on the bit
+           patterns (monotone for positive doubles); halving m lowers its
+           exponent field by one */
+        uint64_t mb = (bits & 0x000FFFFFFFFFFFFFull) | 0x3FF0000000000000ull;
+        uint64_t big = (uint64_t)((int64_t)mb > (int64_t)0x3FF6A09E667F3BCDull);
+        double m = bdbl(mb - (big << 52));
+        double ed = small_int(((bits >> 52) & 0x7FFull)) - 1023.0;
+        ed = ed + small_int(big);
+        double t = (m - 1.0) / (m + 1.0);
+        double t2 = t * t;
+        double s = 1.0 / 19.0;
+        s = s * t2 + 1.0 / 17.0;
+        s = s * t2 + 1.0 / 15.0;
+        s = s * t2 + 1.0 / 13.0;
+        s = s * t2 + 1.0 / 11.0;
+        s = s * t2 + 1.0 / 9.0;
+        s = s * t2 + 1.0 / 7.0;
+        s = s * t2 + 1.0 / 5.0;
+        s = s * t2 + 1.0 / 3.0;
+        s = s * t2 + 1.0;
+        double ln = ed * LN2 + 2.0 * t * s;
+        rad[b] = sqrt(-2.0 * ln);
+        /* cos and sin of 2 pi u2, as in cos_sin_turn; the quadrant is the
+           integer part of 4 u2 */
+        double f = small_int(wo[b]) * INV_2_32;
+        double x = 4.0 * f;
+        int32_t qi = (int32_t)x;
+        double qd = (double)qi;
+        double th = (x - qd) * HALF_PI;
+        double th2 = th * th;
+        double a = -1.0 / 355687428096000.0;
+        a = a * th2 + 1.0 / 1307674368000.0;
+        a = a * th2 - 1.0 / 6227020800.0;
+        a = a * th2 + 1.0 / 39916800.0;
+        a = a * th2 - 1.0 / 362880.0;
+        a = a * th2 + 1.0 / 5040.0;
+        a = a * th2 - 1.0 / 120.0;
+        a = a * th2 + 1.0 / 6.0;
+        a = th - th * th2 * a;
+        double c = 1.0 / 6402373705728000.0;
+        c = c * th2 - 1.0 / 20922789888000.0;
+        c = c * th2 + 1.0 / 87178291200.0;
+        c = c * th2 - 1.0 / 479001600.0;
+        c = c * th2 + 1.0 / 3628800.0;
+        c = c * th2 - 1.0 / 40320.0;
+        c = c * th2 + 1.0 / 720.0;
+        c = c * th2 - 1.0 / 24.0;
+        c = c * th2 + 0.5;
+        c = 1.0 - th2 * c;
+        /* quadrants 0..3: (cos, sin) = (c, a), (-a, c), (-c, -a), (a, -c):
+           swap on odd quadrants, then sign flips, all on the bit patterns */
+        uint64_t q = (uint64_t)(int64_t)qi & 3u;
+        uint64_t swap = 0 - (q & 1u);
+        uint64_t ab = dbits(a), cb = dbits(c);
+        uint64_t cvb = (ab & swap) | (cb & ~swap);
+        uint64_t svb = (cb & swap) | (ab & ~swap);
+        cs[b] = bdbl(cvb ^ (((q ^ (q >> 1)) & 1u) << 63));
+        sn[b] = bdbl(svb ^ ((q >> 1) << 63));
+    }
+}
+
+static void draw_blocks(uint64_t seed, uint64_t stream, uint64_t block0, double z[4 * NB]) {
+    uint32_t w0[NB], w1[NB], w2[NB], w3[NB];
+    const uint32_t s0 = (uint32_t)stream, s1 = (uint32_t)(stream >> 32);
+    for (int b = 0; b < NB; ++b) {
+        uint64_t blk = block0 + (uint64_t)b;
+        uint32_t c0 = (uint32_t)blk, c1 = (uint32_t)(blk >> 32), c2 = s0, c3 = s1;
+        uint32_t ka = (uint32_t)seed, kb = (uint32_t)(seed >> 32);
+        for (int r = 0; r < 10; ++r) {
+            uint64_t p0 = (uint64_t)PHILOX_M0 * c0;
+            uint64_t p1 = (uint64_t)PHILOX_M1 * c2;
+            uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ ka;
+            uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ kb;
+            c0 = n0;
+            c1 = (uint32_t)p1;
+            c2 = n2;
+            c3 = (uint32_t)p0;
+            ka += PHILOX_W0;
+            kb += PHILOX_W1;
+        }
+        w0[b] = c0;
+        w1[b] = c1;
+        w2[b] = c2;
+        w3[b] = c3;
+    }
+    double rad0[NB], cs0[NB], sn0[NB], rad1[NB], cs1[NB], sn1[NB];
+    pair_stage(w0, w1, rad0, cs0, sn0); /* words (x0, x1) of each block */
+    pair_stage(w2, w3, rad1, cs1, sn1); /* words (x2, x3) */
+    for (int b = 0; b < NB; ++b) {
+        z[4 * b + 0] = rad0[b] * cs0[b];
+        z[4 * b + 1] = rad0[b] * sn0[b];
+        z[4 * b + 2] = rad1[b] * cs1[b];
+        z[4 * b + 3] = rad1[b] * sn1[b];
+    }
+}
+
+/*
  * Fill out[0..n) with draws mean + std * N(0,1) of (seed, stream), elements
  * offset .. offset+n of the stream.  kind selects the storage type.
  */
 void synth_normal(uint64_t seed, uint64_t stream, uint64_t offset, uint64_t n, double mean,
                   double std, int kind, void* out) {
-    const int64_t CH = 4096; /* elements per parallel chunk, a multiple of 4 */
+    const int64_t CH = 4 * NB; /* elements per parallel chunk */
     int64_t first_chunk = (int64_t)(offset / CH);
     int64_t last_chunk = n ? (int64_t)((offset + n - 1) / CH) : first_chunk - 1;
 #pragma omp parallel for schedule(static)
     for (int64_t ch = first_chunk; ch <= last_chunk; ++ch) {
-        uint64_t lo = (uint64_t)ch * CH, hi = lo + CH;
-        if (lo < offset) lo = offset;
-        if (hi > offset + n) hi = offset + n;
-        uint64_t i = lo & ~(uint64_t)3;
-        for (; i < hi; i += 4) {
-            uint32_t x[4];
-            philox_block(seed, stream, i >> 2, x);
-            double z[4];
-            box_muller(x[0], x[1], &z[0], &z[1]);
-            box_muller(x[2], x[3], &z[2], &z[3]);
-            for (int j = 0; j < 4; ++j) {
-                uint64_t e = i + (uint64_t)j;
-                if (e < lo || e >= hi) continue;
-                float v = (float)(mean + std * z[j]);
-                uint64_t o = e - offset;
-                if (kind == SYNTH_F32)
-                    ((float*)out)[o] = v;
-                else if (kind == SYNTH_F16)
-                    ((uint16_t*)out)[o] = f32_to_f16_rne(v);
-                else
-                    ((uint16_t*)out)[o] = f32_to_bf16_rne(v);
-            }
+        double z[4 * NB];
+        uint64_t base = (uint64_t)ch * CH;
+        draw_blocks(seed, stream, base >> 2, z);
+        uint64_t lo = base < offset ? offset - base : 0;
+        uint64_t hi = base + CH > offset + n ? offset + n - base : CH;
+        uint64_t o = base + lo - offset;
+        float v[4 * NB];
+        for (uint64_t j = lo; j < hi; ++j) v[j] = (float)(mean + std * z[j]);
+        if (kind == SYNTH_F32) {
+            memcpy((float*)out + o, v + lo, (hi - lo) * sizeof(float));
+        } else if (kind == SYNTH_F16) {
+            uint32_t h[4 * NB]; /* 32-bit lanes for the conversion, narrowed after */
+            for (uint64_t j = lo; j < hi; ++j) h[j] = f32_to_f16_bits32(v[j]);
+            uint16_t* dst = (uint16_t*)out + o;
+            for (uint64_t j = lo; j < hi; ++j) dst[j - lo] = (uint16_t)h[j];
+        } else {
+            uint16_t* dst = (uint16_t*)out + o;
+            for (uint64_t j = lo; j < hi; ++j) dst[j - lo] = f32_to_bf16_rne(v[j]);
         }
     }
 }
