@@ -8,6 +8,8 @@
 * an independent float64 build of the whole decoder from torch.nn.functional
   library routines (layer_norm, linear, scaled_dot_product_attention, relu),
   with LoRA merged into the weights per sequence;
+* exact widening of stored fp16 / bf16 bit patterns to float64, against
+  values fixed by the two formats' definitions;
 * planted mistakes in the oracle are caught by these pins.
 """
 import math
@@ -26,6 +28,8 @@ MINI = synth.Workload(name="mini", seed=101, n_layers=2, d_model=64, n_heads=4, 
                       lora_targets=("q", "k", "v", "o"), lora_rank=4, lora_alpha=8.0,
                       n_adapters=2, adapter_of_seq=(0, -1, 1))
 TINY = synth.WORKLOADS["tiny"]
+# the same decoder stored in bfloat16 (the tiny workload's GPU storage type)
+MINI_BF16 = MINI.with_(name="mini-bf16", dtype="bf16")
 
 
 # ----------------------------------------------------------------------------
@@ -191,6 +195,68 @@ def test_greedy_token_takes_lowest_index_on_ties():
 
 
 # ----------------------------------------------------------------------------
+# widening of stored values (the weights are the fp16 / bf16 values, widened
+# exactly: the model's storage types)
+# ----------------------------------------------------------------------------
+
+# bfloat16 is the top half of an IEEE binary32: sign, 8 exponent bits (bias
+# 127), 7 fraction bits; binary16 has 5 exponent bits (bias 15), 10 fraction bits
+BF16_KNOWN = [
+    (0x0000, 0.0), (0x8000, -0.0), (0x3F80, 1.0), (0xBF80, -1.0), (0xC000, -2.0),
+    (0x3F81, 1.0 + 2.0 ** -7), (0x4049, 3.140625), (0x3C23, 0.00994873046875),
+    (0x0080, 2.0 ** -126),                      # smallest normal
+    (0x0001, 2.0 ** -133),                      # smallest subnormal: 2^-126 * 2^-7
+    (0x007F, (2.0 ** -7) * 127 * 2.0 ** -126),  # largest subnormal
+    (0x7F7F, (2.0 - 2.0 ** -7) * 2.0 ** 127),   # largest finite
+    (0x7F80, math.inf), (0xFF80, -math.inf),
+]
+F16_KNOWN = [
+    (0x0000, 0.0), (0x3C00, 1.0), (0xC000, -2.0), (0x3C01, 1.0 + 2.0 ** -10),
+    (0x0001, 2.0 ** -24), (0x0400, 2.0 ** -14), (0x7BFF, 65504.0), (0x7C00, math.inf),
+    (0xFC00, -math.inf),
+]
+
+
+@pytest.mark.parametrize("kind,table", [("bf16", BF16_KNOWN), ("f16", F16_KNOWN)])
+def test_widen_known_bit_patterns(kind, table):
+    bits = np.array([b for b, _ in table], dtype=np.uint16)
+    got = oracle.widen(bits, kind)
+    for (b, v), g in zip(table, got):
+        assert g == v and math.copysign(1.0, g) == math.copysign(1.0, v), (hex(b), g, v)
+    nan = oracle.widen(np.array([0x7FC0, 0xFFC1, 0x7F81], np.uint16), "bf16")
+    assert np.all(np.isnan(nan))
+
+
+def test_widen_bf16_matches_torch_on_every_pattern():
+    # all 65536 words: torch's bfloat16 -> float64 conversion is an independent
+    # implementation of the same definition
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    got = oracle.widen(bits, "bf16")
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).double().numpy()
+    same = (got == ref) | (np.isnan(got) & np.isnan(ref))
+    assert np.all(same)
+    assert np.array_equal(np.signbit(got), np.signbit(ref))
+
+
+def test_widen_f16_matches_numpy_on_every_pattern():
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    got = oracle.widen(bits, "f16")
+    ref = bits.view(np.float16).astype(np.float64)
+    same = (got == ref) | (np.isnan(got) & np.isnan(ref))
+    assert np.all(same)
+
+
+def test_widen_bf16_is_exact_for_rounded_draws():
+    # a bf16 storage draw widened must equal the float32 draw rounded to bf16
+    f32 = synth.normal(21, 5, (20_000,), 0.0, 0.02, "f32")
+    bf = synth.normal(21, 5, (20_000,), 0.0, 0.02, "bf16")
+    ref = torch.from_numpy(f32).to(torch.bfloat16).double().numpy()
+    assert np.array_equal(oracle.widen(bf, "bf16"), ref)
+    # rounding moves a value by at most half a unit in the last of 8 bits
+    assert np.all(np.abs(oracle.widen(bf, "bf16") - f32) <= np.abs(f32) * 2.0 ** -8)
+
+
+# ----------------------------------------------------------------------------
 # independent float64 build from library routines
 # ----------------------------------------------------------------------------
 
@@ -247,9 +313,9 @@ def torch_prefill(w, toks, adapters):
     return F.linear(z, G["embed"]).numpy()
 
 
-@pytest.mark.parametrize("name", ["mini", "tiny"])
+@pytest.mark.parametrize("name", ["mini", "mini-bf16", "tiny"])
 def test_oracle_matches_independent_library_build(name):
-    w = MINI if name == "mini" else TINY
+    w = {"mini": MINI, "mini-bf16": MINI_BF16, "tiny": TINY}[name]
     toks = synth.tokens(w)
     ad = w.adapters()
     logits, tok = oracle.prefill_first_token(w, tokens=toks)
@@ -313,3 +379,25 @@ def test_planted_mistakes_are_caught(monkeypatch, fname, idx):
     monkeypatch.setattr(ol, fname, MUTANTS[fname][idx])
     logits, _ = ol.prefill_first_token(MINI, tokens=toks)
     assert np.max(np.abs(logits - ref)) > 1e-6
+
+
+def _widen_bf16_shifted(a, kind):
+    # a plausible slip: the bfloat16 word shifted into the wrong half
+    if kind == "bf16":
+        bits = np.asarray(a, dtype=np.uint16).astype(np.uint32) << np.uint32(15)
+        return bits.view(np.float32).astype(np.float64)
+    return _WIDEN(a, kind)
+
+
+_WIDEN = ol.widen
+
+
+def test_planted_widening_mistake_is_caught(monkeypatch):
+    toks = synth.tokens(MINI_BF16)
+    ref = torch_prefill(MINI_BF16, toks, MINI_BF16.adapters())
+    monkeypatch.setattr(ol, "widen", _widen_bf16_shifted)
+    monkeypatch.setattr(oracle, "widen", _widen_bf16_shifted)
+    logits, _ = ol.prefill_first_token(MINI_BF16, tokens=toks)
+    assert not np.all(np.isfinite(logits)) or np.max(np.abs(logits - ref)) > 1e-6
+    with pytest.raises(AssertionError):
+        test_widen_known_bit_patterns("bf16", BF16_KNOWN)
