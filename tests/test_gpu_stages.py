@@ -3,11 +3,14 @@ a contiguous block of layers (streamed as a partial layer order) run their
 block and hand the fp32 hidden states on; the last stage returns the first
 tokens.  Every stage runs the kernels a full prefill would run on its layers,
 so the chain must reproduce one full prefill bit for bit."""
+import os
+
 import numpy as np
 import pytest
 
+import oracle
 import synth
-from gpu_common import log
+from gpu_common import compare, golden_path, log
 
 pytestmark = pytest.mark.gpu
 
@@ -52,6 +55,9 @@ def test_stage_chain_equals_full_prefill(blocks):
             out = m.prefill_stage(toks, ad, b, e, hidden_in=hid if b > 0 else None,
                                   hidden_out=hid if e < W.n_layers else None)
         tok, lg = out
+        # the chain against the oracle's prefill of the same workload
+        o_logits, o_tok = oracle.prefill_first_token(W, tokens=toks, adapter_of_seq=ad)
+        compare("stages %s" % blocks, lg, tok, o_logits, o_tok)
         assert np.array_equal(tok, ref_tok)
         assert np.array_equal(_bits(lg), _bits(ref))
         # a stage on a model that lacks one of its layers fails cleanly
@@ -118,4 +124,41 @@ def test_stage_argument_errors():
         assert e.value.code == pb.PB_EINVAL
     finally:
         m.destroy()
+        hw.free()
+
+
+def test_opt1_3b_two_stage_split_matches_oracle():
+    """OPT-1.3B (24 layers, 512 tokens, LoRA r16 on q,v) run as two stages of
+    one GPU's share: layers 0-11 on one model, 12-23 on another, each loading
+    only its own block; the first token and logits against the oracle's stored
+    logits for the whole model."""
+    import torch
+    from paper_2503_17707_amd import binding as pb
+
+    name = "opt-1.3b"
+    p = golden_path(name)
+    if not os.path.exists(p):
+        pytest.skip("oracle logits for %s not generated" % name)
+    g = np.load(p, allow_pickle=False)
+    w = synth.WORKLOADS[name]
+    log("case stages opt-1.3b 0-11 | 12-23")
+    cfg = pb.make_config(w)
+    hw = pb.HostWeights(w, cfg)
+    models = []
+    try:
+        half = w.n_layers // 2
+        for blk in (range(0, half), range(half, w.n_layers)):
+            m = pb.Model(cfg, "cuda:0")
+            models.append(m)
+            pb.attach_all(m, hw)
+            m.stream_layers(hw, list(blk))
+        toks = synth.tokens(w)
+        ad = list(w.adapters())
+        hid = torch.empty(w.n_tokens, w.d_model, dtype=torch.float32, device="cuda:0")
+        models[0].prefill_stage(toks, ad, 0, half, hidden_out=hid)
+        tok, lg = models[1].prefill_stage(toks, ad, half, w.n_layers, hidden_in=hid)
+        compare("stages opt-1.3b", lg, tok, g["logits"], g["tokens"])
+    finally:
+        for m in models:
+            m.destroy()
         hw.free()
