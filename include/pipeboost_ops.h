@@ -33,6 +33,21 @@ int pb_op_gemm(int32_t dtype, int32_t epi, const void* X, const void* W, const v
                void* C, float* R, int32_t M, int32_t N, int32_t K, float qscale, int32_t qcols,
                void* workspace, size_t workspace_bytes, void* stream);
 
+/* pb_op_gemm for callers that cannot allocate (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the same operands,
+ * epilogues and kernels, with the split-K partials in a 64 MiB device array
+ * of the library instead of a caller workspace.  The call allocates nothing
+ * (no hipMalloc, hipFree or allocating library routine); the array is part
+ * of the library's code object, one copy per GPU, held until the process
+ * ends.  The result is bit-identical to pb_op_gemm given a 64 MiB workspace.
+ * Products are limited to M * N * 4 <= 64 MiB (PB_EINVAL above it: use
+ * pb_op_gemm).  The array of the current device is used, so `stream` must
+ * belong to that device.  Every call on a GPU shares that GPU's array: calls
+ * that overlap on one GPU (other streams or threads) race. */
+int pb_op_gemm_noalloc(int32_t dtype, int32_t epi, const void* X, const void* W, const void* bias,
+                       void* C, float* R, int32_t M, int32_t N, int32_t K, float qscale,
+                       int32_t qcols, void* stream);
+
 /* Causal multi-head self-attention over B sequences of T tokens (Section 2.1:
  * prefill self-attention; token j attends to tokens 0..j).  qkv [B*T, 3*H*hd]
  * dt with q already divided by sqrt(hd), out [B*T, H*hd] dt; hd in {64, 128}. */

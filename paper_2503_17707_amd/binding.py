@@ -118,6 +118,11 @@ _SIGS = {
                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                                   ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_int32,
                                   ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "pb_op_gemm_noalloc": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                          ctypes.c_int32, ctypes.c_float, ctypes.c_int32,
+                                          ctypes.c_void_p]),
     "pb_op_attention": (ctypes.c_int, [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                        ctypes.c_int32, ctypes.c_void_p]),
@@ -579,6 +584,15 @@ def op_gemm(dtype: int, epi: int, X, W, bias, C=None, R=None, qscale: float = 1.
                            qscale, qcols, _ptr(workspace),
                            0 if workspace is None else workspace.numel() * workspace.element_size(),
                            _stream(stream)))
+
+
+def op_gemm_noalloc(dtype: int, epi: int, X, W, bias, C=None, R=None, qscale: float = 1.0,
+                    qcols: int = 0, stream=None):
+    """pb_op_gemm_noalloc: pb_op_gemm with the library's own split-K scratch."""
+    M, K = X.shape
+    N = W.shape[0]
+    check(lib().pb_op_gemm_noalloc(dtype, epi, _ptr(X), _ptr(W), _ptr(bias), _ptr(C), _ptr(R), M, N,
+                                   K, qscale, qcols, _stream(stream)))
 
 
 def op_attention(dtype: int, qkv, out, B: int, T: int, H: int, hd: int, stream=None):

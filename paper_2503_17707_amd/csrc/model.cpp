@@ -1297,9 +1297,11 @@ extern "C" int pb_invalidate_kv(pb_model* m, const uint8_t* layer_lost, int32_t 
 
 #include "../../include/pipeboost_ops.h"
 
-extern "C" int pb_op_gemm(int32_t dtype, int32_t epi, const void* X, const void* W, const void* bias,
-                          void* C, float* R, int32_t M, int32_t N, int32_t K, float qscale,
-                          int32_t qcols, void* workspace, size_t workspace_bytes, void* stream) {
+namespace {
+
+int op_gemm(int32_t dtype, int32_t epi, const void* X, const void* W, const void* bias, void* C, float* R,
+            int32_t M, int32_t N, int32_t K, float qscale, int32_t qcols, const pb::GemmWorkspace& ws,
+            void* stream) {
     if (dtype != PB_BF16 && dtype != PB_F16) return fail(PB_EINVAL, "bad dtype %d", dtype);
     if (epi < 0 || epi > 2) return fail(PB_EINVAL, "epilogue %d not in 0..2", epi);
     if (M < 0 || N <= 0 || K <= 0 || N % 64 || K % 64)
@@ -1310,9 +1312,68 @@ extern "C" int pb_op_gemm(int32_t dtype, int32_t epi, const void* X, const void*
     p.bias = bias; p.C = C; p.ldc = N; p.R = R; p.ldr = N; p.qscale = qscale; p.qcols = qcols;
     const int role = epi == 0 ? 0 : (epi == 1 ? 2 : 3);
     const int e = epi == 0 ? pb::EPI_QKV : (epi == 1 ? pb::EPI_RELU : pb::EPI_RESID);
-    const pb::GemmWorkspace ws{workspace, workspace ? workspace_bytes : 0};
     HIP_TRY(pb::launch_gemm(dtype, role, e, p, ws, (hipStream_t)stream));
     return PB_OK;
+}
+
+}  // namespace
+
+extern "C" int pb_op_gemm(int32_t dtype, int32_t epi, const void* X, const void* W, const void* bias,
+                          void* C, float* R, int32_t M, int32_t N, int32_t K, float qscale,
+                          int32_t qcols, void* workspace, size_t workspace_bytes, void* stream) {
+    const pb::GemmWorkspace ws{workspace, workspace ? workspace_bytes : 0};
+    return op_gemm(dtype, epi, X, W, bias, C, R, M, N, K, qscale, qcols, ws, stream);
+}
+
+// ---- pb_op_gemm without a caller workspace and without allocating ----------
+// The split-K partials go to `scratch`, a device array of this file that every
+// GPU the library runs on holds (its own copy, at its own address) until the
+// process ends.  In host code the name `scratch` is only the host-side stand-in
+// of the array: its device address comes from hipGetSymbolAddress, taken once
+// per device with that device current, and only that address is ever handed to
+// kernels.  Nothing in the array needs to start at zero: every split writes its
+// whole partial tile before the reduce reads it.  Calls on one GPU share the
+// array, so calls that overlap on that GPU (other streams, other threads) race.
+
+namespace {
+
+constexpr size_t NOALLOC_SCRATCH_BYTES = size_t(64) << 20;
+constexpr int NOALLOC_MAX_DEVICES = 64;
+
+__device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
+
+std::mutex g_scratch_mu;
+void* g_scratch_dev[NOALLOC_MAX_DEVICES] = {};  // device address of `scratch`, per device
+
+}  // namespace
+
+extern "C" int pb_op_gemm_noalloc(int32_t dtype, int32_t epi, const void* X, const void* W,
+                                  const void* bias, void* C, float* R, int32_t M, int32_t N, int32_t K,
+                                  float qscale, int32_t qcols, void* stream) {
+    if (M < 0 || N <= 0) return fail(PB_EINVAL, "shape M=%d N=%d", M, N);
+    if ((size_t)M * (size_t)N * 4 > NOALLOC_SCRATCH_BYTES)
+        return fail(PB_EINVAL,
+                    "pb_op_gemm_noalloc: M*N*4 = %zu bytes exceeds the %zu-byte scratch (M*N <= %zu); "
+                    "use pb_op_gemm with a workspace",
+                    (size_t)M * (size_t)N * 4, NOALLOC_SCRATCH_BYTES, NOALLOC_SCRATCH_BYTES / 4);
+    int dev = -1;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= NOALLOC_MAX_DEVICES) return fail(PB_EINVAL, "device %d out of range", dev);
+    void* ptr = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_scratch_mu);
+        if (!g_scratch_dev[dev]) {
+            void* a = nullptr;
+            const hipError_t e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+            if (e != hipSuccess || !a)
+                return fail(PB_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                            hipGetErrorString(e));
+            g_scratch_dev[dev] = a;
+        }
+        ptr = g_scratch_dev[dev];
+    }
+    const pb::GemmWorkspace ws{ptr, NOALLOC_SCRATCH_BYTES};
+    return op_gemm(dtype, epi, X, W, bias, C, R, M, N, K, qscale, qcols, ws, stream);
 }
 
 extern "C" int pb_op_attention(int32_t dtype, const void* qkv, void* out, int32_t B, int32_t T,
