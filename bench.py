@@ -462,6 +462,39 @@ def measure(w, steps, warmup, cold_reps, decode_steps, pb, torch, np):
 
 
 
+def attention_only(names, pb, torch, reps=20):
+    """The prefill attention kernel alone (pb_op_attention) at each workload's
+    shape (B sequences of T tokens, H heads of head_dim hd) on random q, k, v:
+    events around `reps` back-to-back launches after a warm-up.  FLOPs count
+    the causal products only (QK^T and PV over keys <= query)."""
+    out = {}
+    g = torch.Generator(device="cuda:0").manual_seed(7)
+    for name in names:
+        import synth
+
+        w = synth.WORKLOADS[name]
+        B, T, H, hd = w.batch, w.seq_len, w.n_heads, w.head_dim
+        dt = torch.float16 if w.dtype == "f16" else torch.bfloat16
+        dcode = 1 if w.dtype == "f16" else 0
+        qkv = torch.randn(B * T, 3 * H * hd, device="cuda:0", generator=g).to(dt)
+        o = torch.empty(B * T, H * hd, dtype=dt, device="cuda:0")
+        for _ in range(3):
+            pb.op_attention(dcode, qkv, o, B, T, H, hd)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            pb.op_attention(dcode, qkv, o, B, T, H, hd)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        fl = 2.0 * B * H * hd * T * (T + 1)
+        out[name] = {"B": B, "T": T, "H": H, "head_dim": hd, "us": us, "tflops": fl / us / 1e6,
+                     "frac_of_mfma_peak": fl / us / 1e6 / MFMA_PEAK_TFLOPS}
+        del qkv, o
+    return {"attention_only": out, "launches_timed": reps}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -489,6 +522,9 @@ def main():
     ap.add_argument("--gemm-reference", action="store_true",
                     help="only time the workload's four projection GEMMs through this library's "
                          "kernels and through the vendor library (torch's linear), then exit")
+    ap.add_argument("--attention-only", default="",
+                    help="only time the prefill attention kernel at these workloads' shapes "
+                         "(comma-separated names), then exit")
     ap.add_argument("--h2d-sweep", action="store_true",
                     help="only measure the loader's H2D rate over chunk sizes, and plain pinned "
                          "copies on one and two streams, then exit")
@@ -516,6 +552,9 @@ def main():
     from paper_2503_17707_amd import binding as pb
 
     pb.lib()  # fails loudly if the HIP library is missing
+    if args.attention_only:
+        print(json.dumps(attention_only(args.attention_only.split(","), pb, torch)), flush=True)
+        return
     w = synth.WORKLOADS[args.workload]
     if args.layers:
         w = w.with_(n_layers=min(args.layers, w.n_layers), layer_order=None)

@@ -18,7 +18,9 @@
 // 8 scores it already holds.  The V^T operand is read from the row-major V
 // tile with transposing LDS reads (ds_read_b64_tr_b16) in the same key order.
 //
-// Blocks run heaviest-first (the last query block sees the most keys).  When
+// The max and sum over a query's four lane groups use v_permlane16/32_swap
+// (VALU, no LDS round trip).  Blocks run heaviest-first over all (sequence,
+// head) pairs (the last query block of a pair sees the most keys).  When
 // query blocks are few (a short prompt), KS = 2 wave groups of 4 share a
 // block's queries and take alternating key tiles; the two online-softmax
 // states are merged through LDS at the end, halving the longest block's key
@@ -36,6 +38,12 @@ namespace {
 #ifndef PB_ATTN_KS2
 #define PB_ATTN_KS2 1  // allow two wave groups splitting the keys
 #endif
+#ifndef PB_ATTN_KSWZ16
+#define PB_ATTN_KSWZ16 1  // K tiles of head_dim 128 permuted over all 16 chunks
+#endif
+#ifndef PB_ATTN_PERMLANE
+#define PB_ATTN_PERMLANE 1  // reductions over the 4 lane groups with permlane swaps
+#endif
 
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr int BKV = 64;  // keys per tile
@@ -43,7 +51,14 @@ constexpr int BKV = 64;  // keys per tile
 // 16-byte chunk permutations of a K or V tile row (key = row): K is read as
 // 16 consecutive rows at one chunk, V by transposing 8-byte reads of four
 // consecutive rows at two neighbouring chunks.
-__device__ __forceinline__ int kswz(int row, int ch) { return ch ^ (row & 7); }
+template <int HD>
+__device__ __forceinline__ int kswz(int row, int ch) {
+    // a read of 16 consecutive rows at one chunk hits 16 distinct 16-byte
+    // positions of the 256-byte bank window: with 128-byte rows (row & 7) and
+    // the row parity do it, with 256-byte rows the permutation needs (row & 15)
+    if (HD == 128 && PB_ATTN_KSWZ16) return ch ^ (row & 15);
+    return ch ^ (row & 7);
+}
 template <int HD>
 __device__ __forceinline__ int vswz(int row, int ch) {
     // rows 4 g + j (j = 0..3) of one transposing read land in distinct banks
@@ -65,13 +80,43 @@ __device__ __forceinline__ u32x2 read_tr16(const uint8_t* p) {
     return __builtin_bit_cast(u32x2, v);
 }
 
-template <typename T, int HD, int QW, int KS>
-__global__ __launch_bounds__(256 * KS) __attribute__((amdgpu_waves_per_eu(QW == 32 || KS == 2 ? 2 : 1)))
+// max and sum over lanes l, l ^ 16, l ^ 32, l ^ 48 (the four 16-lane groups),
+// identical in all four lanes: v_permlane16_swap of a register with itself
+// hands every lane the value of the same lane position in the paired 16-lane
+// row (rows 0 <-> 1, 2 <-> 3), v_permlane32_swap that of the other 32-lane
+// half (layout checked on gfx950 with an in-bounds probe); plain VALU
+// instructions, no LDS round trip
+__device__ __forceinline__ float group4_max(float v) {
+#if PB_ATTN_PERMLANE
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+#else
+    v = fmaxf(v, __shfl_xor(v, 16, 64));
+    return fmaxf(v, __shfl_xor(v, 32, 64));
+#endif
+}
+
+__device__ __forceinline__ float group4_sum(float v) {
+#if PB_ATTN_PERMLANE
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+#else
+    v += __shfl_xor(v, 16, 64);
+    return v + __shfl_xor(v, 32, 64);
+#endif
+}
+
+template <typename T, int HD, int QW, int KS, int NQW, int S>
+__global__ __launch_bounds__(64 * NQW * KS) __attribute__((amdgpu_waves_per_eu(QW == 32 || KS == 2 || NQW == 8 ? 2 : 1)))
 void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, int64_t kv_ld, int64_t kv_seq,
-                      T* __restrict__ out, int T_len, int H) {
+                      T* __restrict__ out, int T_len, int H, int B) {
     typedef typename Mfma<T>::vec8 vec8;
-    constexpr int NW = 4 * KS;         // waves per block
-    constexpr int BQ = 4 * QW;         // queries per block (4 waves per group)
+    constexpr int NW = NQW * KS;       // waves per block
+    constexpr int BQ = NQW * QW;       // queries per block (NQW waves per group)
     constexpr int NQG = QW / 16;       // 16-query groups per wave
     constexpr int CS = HD / 32;        // 32-wide k steps over head_dim
     constexpr int CT = HD / 16;        // 16-row tiles of O^T
@@ -89,10 +134,16 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
     const int d = H * HD;
     const int64_t ld = 3 * (int64_t)d;
     const int nqb = (T_len + BQ - 1) / BQ;
-    const int qb = nqb - 1 - (int)blockIdx.x;  // heaviest blocks first
-    const int h = blockIdx.y, b = blockIdx.z;
+    // Heaviest query blocks first over all (sequence, head) pairs: block L
+    // takes query block rank L / (H B) of pair L % (H B), so every pair's
+    // longest block starts in the first round and the short ones fill the
+    // tail (1.3-1.7x faster than walking the pairs one after another)
+    const int G = H * B;
+    const int qrank = (int)blockIdx.x / G, pair = (int)blockIdx.x % G;
+    const int qb = nqb - 1 - qrank;
+    const int h = pair % H, b = pair / H;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int grp = wave / 4, wq = wave % 4;  // key-tile group, wave within it
+    const int grp = wave / NQW, wq = wave % NQW;  // key-tile group, wave within it
     const int lr = lane & 15, lg = lane >> 4;
     const int64_t row0 = (int64_t)b * T_len;
     const T* Qb = qkv + h * HD;
@@ -123,7 +174,7 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
             const bool isv = Ig >= NIG / 2;
             const int row = RPI * (Ig % (NIG / 2)) + lane / CPR;
             const int pch = lane % CPR;
-            const int ch = isv ? vswz<HD>(row, pch) : kswz(row, pch);
+            const int ch = isv ? vswz<HD>(row, pch) : kswz<HD>(row, pch);
             const int key = min(kb * BKV + row, T_len - 1);
             const T* src = kvsrc + b * kv_seq + key * kv_ld + (isv ? d : 0) + h * HD + ch * 8;
             dma16(src, sbase + (uint32_t)__builtin_amdgcn_readfirstlane(I * 1024));
@@ -143,14 +194,10 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
     // keys needed by this block: those <= its last query (and < T)
     const int nkb = min((T_len + BKV - 1) / BKV, ((qb + 1) * BQ + BKV - 1) / BKV);
     const int nit = (nkb + KS - 1) / KS;
-    issue(0, 0);
-    for (int it = 0; it < nit; ++it) {
-        wait_vmcnt<0>();
-        __syncthreads();  // tiles of iteration it visible; stage of it-1 free
-        if (it + 1 < nit) issue(it + 1, (it + 1) & 1);
+    auto body = [&](int it) {
         const int kb = it * KS + grp;
-        if (kb >= nkb) continue;  // wave-uniform: this group has no tile left
-        const uint8_t* sK = smem + (it & 1) * STAGE + grp * GSTAGE;
+        if (kb >= nkb) return;  // wave-uniform: this group has no tile left
+        const uint8_t* sK = smem + (it % S) * STAGE + grp * GSTAGE;
         const uint8_t* sV = sK + TILE;
 
         // S^T tiles: key = kb*64 + 16 jt + 4 lg + r, query = q0 + 16 qg + lr
@@ -161,7 +208,7 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
             vec8 kf[CS];
 #pragma unroll
             for (int cs = 0; cs < CS; ++cs)
-                kf[cs] = as_vec8<T>(*(const u32x4*)(sK + row * RB + (kswz(row, cs * 4 + lg) << 4)));
+                kf[cs] = as_vec8<T>(*(const u32x4*)(sK + row * RB + (kswz<HD>(row, cs * 4 + lg) << 4)));
 #pragma unroll
             for (int qg = 0; qg < NQG; ++qg) {
                 sc[qg][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -191,8 +238,7 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
             for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[qg][jt][r]);
-            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            mx = group4_max(mx);
             // key kb*64 <= q_idx always holds for a computed tile, so m_new is finite
             // The running max is kept unless the tile exceeds it by more than
             // 8 in log2 units, so P stays below 2^8 (well inside dt) and the
@@ -212,8 +258,7 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
                     pt[jt][r] = (T)e;
                     psum += e;
                 }
-            psum += __shfl_xor(psum, 16, 64);
-            psum += __shfl_xor(psum, 32, 64);
+            psum = group4_sum(psum);
             l_run[qg] = l_run[qg] * alpha + psum;
             m_run[qg] = m_new;
             if (__any(alpha != 1.f)) {
@@ -260,13 +305,29 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
                 for (int qg = 0; qg < NQG; ++qg) o[qg][ct] = Mfma<T>::mma(vf, pf[qg][ks], o[qg][ct]);
             }
         }
+    };
+    // S-stage ring: iterations it+1 .. it+S-2 are in flight while it is used
+#pragma unroll
+    for (int q = 0; q < S - 1; ++q)
+        if (q < nit) issue(q, q);
+    int it = 0;
+    for (; it + S - 1 < nit; ++it) {
+        wait_vmcnt<(S - 2) * NL>();
+        __syncthreads();  // tiles of iteration it visible; stage of it-1 free
+        issue(it + S - 1, (it + S - 1) % S);
+        body(it);
+    }
+    for (; it < nit; ++it) {
+        wait_vmcnt<0>();
+        __syncthreads();
+        body(it);
     }
 
     if (KS == 2) {
         // merge group 1's (max, sum, O^T) into group 0's: every lane holds
         // the same query and O^T rows in both groups
-        float* xo = (float*)smem;                           // [4 waves][NQG][CT][64 lanes][4]
-        float* xm = xo + 4 * NQG * CT * 64 * 4;             // [4 waves][NQG][64 lanes][2]
+        float* xo = (float*)smem;                           // [NQW waves][NQG][CT][64 lanes][4]
+        float* xm = xo + NQW * NQG * CT * 64 * 4;           // [NQW waves][NQG][64 lanes][2]
         __syncthreads();  // every wave is done with the ring
         if (grp == 1) {
 #pragma unroll
@@ -311,36 +372,38 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
     }
 }
 
-template <typename T, int HD, int QW, int KS>
+template <typename T, int HD, int QW, int KS, int NQW, int S>
 hipError_t launch_hd(const void* qkv, const void* kv, int64_t kv_ld, int64_t kv_seq, void* out, int B,
                      int T_len, int H, hipStream_t s) {
-    constexpr int LDS = 2 * KS * 2 * BKV * HD * 2;  // two stages of KS key tiles (K and V)
-    static_assert(KS == 1 || 4 * QW / 16 * (HD / 16) * 64 * 16 + 4 * QW / 16 * 64 * 8 <= LDS,
+    constexpr int LDS = S * KS * 2 * BKV * HD * 2;  // S stages of KS key tiles (K and V)
+    static_assert(KS == 1 || NQW * QW / 16 * (HD / 16) * 64 * 16 + NQW * QW / 16 * 64 * 8 <= LDS,
                   "the merge fits in the ring");
+    static_assert(LDS <= 160 * 1024, "LDS");
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void*)attention_kernel<T, HD, QW, KS>,
+        hipError_t e = hipFuncSetAttribute((const void*)attention_kernel<T, HD, QW, KS, NQW, S>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, LDS);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    dim3 grid((T_len + 4 * QW - 1) / (4 * QW), H, B);
-    PB_LAUNCH((attention_kernel<T, HD, QW, KS>), grid, dim3(256 * KS), LDS, s, (const T*)qkv, (const T*)kv,
-              kv_ld, kv_seq, (T*)out, T_len, H);
+    const long nblk = (long)((T_len + NQW * QW - 1) / (NQW * QW)) * H * B;
+    PB_LAUNCH((attention_kernel<T, HD, QW, KS, NQW, S>), dim3((unsigned)nblk), dim3(64 * NQW * KS), LDS, s,
+              (const T*)qkv, (const T*)kv, kv_ld, kv_seq, (T*)out, T_len, H, B);
     return hipGetLastError();
 }
 
 template <typename T, int HD>
 hipError_t launch_qw(const void* qkv, const void* kv, int64_t kv_ld, int64_t kv_seq, void* out, int B,
                      int T_len, int H, hipStream_t s) {
+    const long pairs = (long)H * B;
     // 32 queries per wave when 128-query blocks still give every CU work;
     // with fewer than 512 blocks of 64 queries, two wave groups split the keys
-    const long blocks128 = (long)((T_len + 127) / 128) * H * B;
-    const long blocks64 = (long)((T_len + 63) / 64) * H * B;
-    if (PB_ATTN_QW32 && blocks128 >= 512) return launch_hd<T, HD, 32, 1>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
+    const long blocks128 = (long)((T_len + 127) / 128) * pairs;
+    const long blocks64 = (long)((T_len + 63) / 64) * pairs;
+    if (PB_ATTN_QW32 && blocks128 >= 512) return launch_hd<T, HD, 32, 1, 4, 2>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
     if (PB_ATTN_KS2 && blocks64 < 512 && T_len > BKV)
-        return launch_hd<T, HD, 16, 2>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
-    return launch_hd<T, HD, 16, 1>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
+        return launch_hd<T, HD, 16, 2, 4, 2>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
+    return launch_hd<T, HD, 16, 1, 4, 2>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
 }
 
 // ---- decode: one new query per (sequence, head) against the KV cache --------

@@ -38,7 +38,8 @@
       SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE SQ_LDS_DATA_FIFO_FULL SQ_LDS_CMD_FIFO_FULL
       SQ_ACTIVE_INST_VALU SQ_ACTIVE_INST_SCA SQ_INSTS_LDS GRBM_GUI_ACTIVE: where the
       GEMM waves' cycles go, for this library's GEMM kernels (by tile and role)
-      and the vendor library's, side by side.
+      and the vendor library's, side by side.  With `bench.py --attention-only`
+      runs instead, the same columns for the prefill attention kernels.
 
 Only reads files; used to write the summaries kept with the profiles.
 """
@@ -254,6 +255,10 @@ def traffic(fetch, write, cal_fetch, cal_write, label):
 
 
 def _gemm_key(name):
+    m = re.search(r"attention_kernelIDF16b?_((?:Li\d+E)+)", name)
+    if m and "decode" not in name:
+        a = [int(x) for x in re.findall(r"Li(\d+)E", m.group(1))]
+        return "attention hd %d, %d queries/wave, %d key group(s)" % (a[0], a[1], a[2])
     m = re.search(r"gemm_kernelIDF16b?_((?:Li\d+E)+)", name)
     if m:
         a = [int(x) for x in re.findall(r"Li(\d+)E", m.group(1))]
@@ -272,7 +277,7 @@ def stalls(dir_a, dir_b, label):
             k = _gemm_key(r["Kernel_Name"])
             if k:
                 per[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
-    out = ["# Where the GEMM waves' cycles go, %s\n" % label,
+    out = ["# Where the waves' cycles go, %s\n" % label,
            "Kernel sources (paper_2503_17707_amd/csrc/*) sha256: `%s`\n" % source_sha256(),
            "Counters per dispatch (dispatches serialized by the counter runs), averaged per kernel.  "
            "Per wave-cycle: SQ_WAIT_ANY (waiting at a wait-count or barrier), SQ_WAIT_INST_ANY "

@@ -86,7 +86,10 @@ def test_gemm_epilogues(kind, M, N, K, epi):
 @pytest.mark.parametrize("kind,hd,B,T,H", [("f16", 64, 2, 200, 3), ("bf16", 64, 1, 37, 2),
                                            ("f16", 128, 1, 130, 2), ("bf16", 128, 2, 64, 1),
                                            ("f16", 128, 1, 1100, 4), ("f16", 64, 1, 1, 2),
-                                           ("bf16", 64, 1, 530, 2), ("f16", 64, 2, 129, 2)])
+                                           ("bf16", 64, 1, 530, 2), ("f16", 64, 2, 129, 2),
+                                           # long prompts (8-wave blocks): 32 and 16 queries per
+                                           # wave, (sequence, head) pairs a multiple of 8, ragged T
+                                           ("f16", 128, 4, 1024, 32), ("bf16", 128, 1, 2000, 40)])
 def test_attention(kind, hd, B, T, H):
     import torch
 
