@@ -44,7 +44,10 @@ DT = {"bf16": 0, "f16": 1}
                                    (1030, 768, 512), (1, 64, 64),
                                    # at most 8 rows: the weight-streaming path, K ragged
                                    # against its 1024-column steps
-                                   (1, 2048, 2048), (3, 576, 1600), (8, 128, 8192)])
+                                   (1, 2048, 2048), (3, 576, 1600), (8, 128, 8192),
+                                   # 256 x 256 tiles: many tiles with a ragged M, and few
+                                   # tiles over a long K (split along K)
+                                   (4000, 4096, 512), (2048, 2048, 8192)])
 @pytest.mark.parametrize("epi", [0, 1, 2])
 def test_gemm_epilogues(kind, M, N, K, epi):
     import torch
@@ -57,7 +60,7 @@ def test_gemm_epilogues(kind, M, N, K, epi):
     b = _draw(71, 3, (N,), 0.02, kind)
     Xd, Wd, bd = _dev(X, kind), _dev(W, kind), _dev(b, kind)
     ref = oracle.widen(X, kind) @ oracle.widen(W, kind).T + oracle.widen(b, kind)
-    ws = torch.empty(16 << 20, dtype=torch.uint8, device="cuda")
+    ws = torch.empty(max(16 << 20, min(256 << 20, 16 * M * N)), dtype=torch.uint8, device="cuda")
     if epi == 2:
         R0 = synth.normal(71, 4, (M, N), 0.0, 1.0, "f32")
         R = torch.from_numpy(R0.copy()).cuda()
