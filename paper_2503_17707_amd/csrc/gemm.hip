@@ -66,6 +66,9 @@ namespace {
 #ifndef PB_GEMM_S256
 #define PB_GEMM_S256 2  // ... of the 256 x 256 tiles
 #endif
+#ifndef PB_GEMM_RAGGED
+#define PB_GEMM_RAGGED 1  // split only the tail tiles of a ragged last round
+#endif
 
 constexpr int BK = 64;
 constexpr int ROW_BYTES = BK * 2;
@@ -123,6 +126,12 @@ struct SplitArgs {
     int splits;     // number of K splits (1 = none)
     int kt_split;   // K tiles per split (the LoRA tiles go to the last split)
     float* ws;      // [splits][M][N] fp32 partials when splits > 1
+    // ragged-round split (full_tiles > 0): tiles [0, full_tiles) run whole
+    // through the epilogue, only the tail tiles [full_tiles, full_tiles +
+    // tail_tiles) are split `splits` ways, their partials packed as
+    // [split][tail tile][BM][BN]; full_tiles and tail_tiles * splits are
+    // multiples of 8
+    int full_tiles, tail_tiles;
 };
 
 // Which output tile and K range a block works on: the hardware deals
@@ -133,8 +142,24 @@ struct SplitArgs {
 // also the LoRA K tiles of its output group (if that group is active).
 struct TileJob {
     int m0, n0, split, nk1, t_begin, nk;
+    bool partial;    // writes an fp32 partial tile (split along K) instead of the epilogue
+    float* pbase;    // ... at pbase + (m - om) * ldp + (n - on)
+    int ldp, om, on;
     const void* X2;  // LoRA activations of the tile's output group
 };
+
+// Output tile index -> its corner: tiles are walked in groups of GROUP_M
+// tile-rows (blocks that share an XCD's L2 share rows of X and of W).
+template <int BM, int BN>
+__device__ __forceinline__ void tile_corner(const GemmParams& p, int tile, int& m0, int& n0) {
+    const int tiles_m = (p.M + BM - 1) / BM;
+    const int tiles_n = (p.N + BN - 1) / BN;
+    const int per_group = GROUP_M * tiles_n;
+    const int first_m = (tile / per_group) * GROUP_M;
+    const int gsize = min(tiles_m - first_m, GROUP_M);
+    m0 = (first_m + (tile % per_group) % gsize) * BM;
+    n0 = ((tile % per_group) / gsize) * BN;
+}
 
 template <int BM, int BN>
 __device__ __forceinline__ TileJob tile_job(const GemmParams& p, const SplitArgs& sa) {
@@ -143,15 +168,43 @@ __device__ __forceinline__ TileJob tile_job(const GemmParams& p, const SplitArgs
     const int tiles = tiles_m * tiles_n;
     int bid = blockIdx.x;
     const int nblk = gridDim.x;
-    if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
-    const int tile = bid % tiles, split = bid / tiles;
-    const int per_group = GROUP_M * tiles_n;
-    const int first_m = (tile / per_group) * GROUP_M;
-    const int gsize = min(tiles_m - first_m, GROUP_M);
+    int tile, split;
+    bool partial;
+    if (sa.full_tiles > 0) {
+        // the whole tiles first, then the split tail tiles, each part dealt
+        // XCD-contiguously on its own so that the tail round spreads over all
+        // eight XCDs
+        if (bid < sa.full_tiles) {
+            tile = (sa.full_tiles & 7) ? bid : (bid & 7) * (sa.full_tiles >> 3) + (bid >> 3);
+            split = 0;
+            partial = false;
+        } else {
+            const int r = bid - sa.full_tiles, nt = nblk - sa.full_tiles;
+            const int rr = (nt & 7) ? r : (r & 7) * (nt >> 3) + (r >> 3);
+            tile = sa.full_tiles + rr % sa.tail_tiles;
+            split = rr / sa.tail_tiles;
+            partial = true;
+        }
+    } else {
+        if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
+        tile = bid % tiles;
+        split = bid / tiles;
+        partial = sa.splits > 1;
+    }
     TileJob j;
-    j.m0 = (first_m + (tile % per_group) % gsize) * BM;
-    j.n0 = ((tile % per_group) / gsize) * BN;
+    tile_corner<BM, BN>(p, tile, j.m0, j.n0);
     j.split = split;
+    j.partial = partial;
+    if (sa.full_tiles > 0) {
+        j.pbase = sa.ws + ((int64_t)split * sa.tail_tiles + (tile - sa.full_tiles)) * (BM * BN);
+        j.ldp = BN;
+        j.om = j.m0;
+        j.on = j.n0;
+    } else {
+        j.pbase = sa.ws + (int64_t)split * p.M * p.N;
+        j.ldp = p.N;
+        j.om = j.on = 0;
+    }
     j.nk1 = p.K1 / BK;
     int nk2 = 0;
     j.X2 = p.X2;
@@ -162,17 +215,22 @@ __device__ __forceinline__ TileJob tile_job(const GemmParams& p, const SplitArgs
             j.X2 = (const char*)p.X2 + (int64_t)g * p.x2_group_stride * 2;
         }
     }
-    j.t_begin = split * sa.kt_split;
-    const int t_end = (split == sa.splits - 1) ? j.nk1 + nk2 : min(j.nk1, j.t_begin + sa.kt_split);
-    j.nk = t_end - j.t_begin;
+    if (!partial) {
+        j.t_begin = 0;
+        j.nk = j.nk1 + nk2;
+    } else {
+        j.t_begin = split * sa.kt_split;
+        const int t_end = (split == sa.splits - 1) ? j.nk1 + nk2 : min(j.nk1, j.t_begin + sa.kt_split);
+        j.nk = t_end - j.t_begin;
+    }
     return j;
 }
 
 // Epilogue of a wave's accumulators: acc[i][j] holds output features
 // nb + 16 i + 4 lg + r (r = 0..3) of token mb + 16 j + lr.
 template <typename T, int EPI, int MF, int NF>
-__device__ __forceinline__ void store_tile(const GemmParams& p, const SplitArgs& sa, int split, int mb, int nb,
-                                           int lr, int lg, const f32x4 (&acc)[NF][MF]) {
+__device__ __forceinline__ void store_tile(const GemmParams& p, const TileJob& jb, int mb, int nb, int lr, int lg,
+                                           const f32x4 (&acc)[NF][MF]) {
 #pragma unroll
     for (int j = 0; j < MF; ++j) {
         const int m = mb + j * 16 + lr;
@@ -181,8 +239,8 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, const SplitArgs&
         for (int i = 0; i < NF; ++i) {
             const int n = nb + i * 16 + 4 * lg;
             if (n >= p.N) continue;
-            if (sa.splits > 1)
-                *(f32x4*)(sa.ws + ((int64_t)split * p.M + m) * p.N + n) = acc[i][j];
+            if (jb.partial)
+                *(f32x4*)(jb.pbase + (int64_t)(m - jb.om) * jb.ldp + (n - jb.on)) = acc[i][j];
             else
                 epilogue4<T, EPI>(p, m, n, acc[i][j]);
         }
@@ -209,7 +267,7 @@ void gemm_kernel(GemmParams p, SplitArgs sa) {
     const int lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WGM, wn = wave / WGM;
     const TileJob jb = tile_job<BM, BN>(p, sa);
-    const int m0 = jb.m0, n0 = jb.n0, split = jb.split, nk1 = jb.nk1, t_begin = jb.t_begin, nk = jb.nk;
+    const int m0 = jb.m0, n0 = jb.n0, nk1 = jb.nk1, t_begin = jb.t_begin, nk = jb.nk;
     const T* X2 = (const T*)jb.X2;
 
     // DMA instruction j of this wave fills LDS rows 8g .. 8g+7, g = wave + NW j;
@@ -289,7 +347,7 @@ void gemm_kernel(GemmParams p, SplitArgs sa) {
         compute(t % S);
     }
 
-    store_tile<T, EPI, MF, NF>(p, sa, split, m0 + wm * WM, n0 + wn * WN, lr, lg, acc);
+    store_tile<T, EPI, MF, NF>(p, jb, m0 + wm * WM, n0 + wn * WN, lr, lg, acc);
 }
 
 // Sum the split-K partials in split order, then apply the epilogue.
@@ -301,6 +359,32 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmParams p, SplitA
     const int m = (int)(q / per_row), n = (int)(q % per_row) * 4;
     const int64_t stride = (int64_t)p.M * p.N;
     const float* src = sa.ws + (int64_t)m * p.N + n;
+    f32x4 v = *(const f32x4*)src;
+    for (int s = 1; s < sa.splits; ++s) {
+        const f32x4 w = *(const f32x4*)(src + s * stride);
+        v[0] += w[0];
+        v[1] += w[1];
+        v[2] += w[2];
+        v[3] += w[3];
+    }
+    epilogue4<T, EPI>(p, m, n, v);
+}
+
+// Reduce of a ragged-round split: only the tail tiles' partials, summed in
+// split order, then the epilogue.  One thread per group of 4 columns.
+template <typename T, int EPI, int ROLE, int BM, int BN>
+__global__ __launch_bounds__(256) void tail_reduce_kernel(GemmParams p, SplitArgs sa) {
+    constexpr int GPT = BM * BN / 4;  // column groups per tile
+    const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (q >= (int64_t)sa.tail_tiles * GPT) return;
+    const int tt = (int)(q / GPT);
+    int m0, n0;
+    tile_corner<BM, BN>(p, sa.full_tiles + tt, m0, n0);
+    const int e = (int)(q % GPT);
+    const int m = m0 + e / (BN / 4), n = n0 + (e % (BN / 4)) * 4;
+    if (m >= p.M || n >= p.N) return;
+    const int64_t stride = (int64_t)sa.tail_tiles * BM * BN;
+    const float* src = sa.ws + (int64_t)tt * BM * BN + (int64_t)(m - m0) * BN + (n - n0);
     f32x4 v = *(const f32x4*)src;
     for (int s = 1; s < sa.splits; ++s) {
         const f32x4 w = *(const f32x4*)(src + s * stride);
@@ -409,6 +493,7 @@ SplitArgs make_split(const GemmParams& p, const GemmWorkspace& wsp, int splits) 
     sa.kt_split = (nk1 + splits - 1) / splits;
     sa.splits = (nk1 + sa.kt_split - 1) / sa.kt_split;
     sa.ws = (float*)wsp.ws;
+    sa.full_tiles = sa.tail_tiles = 0;
     return sa;
 }
 
@@ -428,7 +513,7 @@ hipError_t finish_split(const GemmParams& p, const SplitArgs& sa, hipStream_t s)
 }
 
 template <typename T, int EPI, int BM, int BN, int WGM, int WGN, int ROLE, int S>
-hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, int splits, hipStream_t s) {
+hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, int splits, int ragged_tail, hipStream_t s) {
     constexpr int LDS = S * (BM + BN) * ROW_BYTES;
     static bool attr_set = false;
     if (!attr_set) {
@@ -438,7 +523,23 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, int splits,
         attr_set = true;
     }
     const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
-    const SplitArgs sa = make_split(p, wsp, splits);
+    SplitArgs sa = make_split(p, wsp, splits);
+    if (ragged_tail > 0) {
+        if (sa.splits >= 2 && (tiles - ragged_tail) % 8 == 0 && (ragged_tail * sa.splits) % 8 == 0) {
+            // whole tiles, then the tail split (sa.splits ways)
+            sa.full_tiles = tiles - ragged_tail;
+            sa.tail_tiles = ragged_tail;
+            PB_LAUNCH((gemm_kernel<T, EPI, BM, BN, WGM, WGN, ROLE, S>),
+                      dim3(sa.full_tiles + ragged_tail * sa.splits), dim3(64 * WGM * WGN), LDS, s, p, sa);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            const int64_t groups = (int64_t)ragged_tail * (BM * BN / 4);
+            PB_LAUNCH((tail_reduce_kernel<T, EPI, ROLE, BM, BN>), dim3((unsigned)((groups + 255) / 256)), dim3(256), 0,
+                      s, p, sa);
+            return hipGetLastError();
+        }
+        sa = make_split(p, wsp, 1);  // the split did not come out as planned: whole tiles only
+    }
     PB_LAUNCH((gemm_kernel<T, EPI, BM, BN, WGM, WGN, ROLE, S>), dim3(tiles * sa.splits),
                        dim3(64 * WGM * WGN), LDS, s, p, sa);
     const hipError_t e = hipGetLastError();
@@ -454,24 +555,42 @@ hipError_t launch_cfg(const GemmParams& p, const GemmWorkspace& wsp, int splits,
 struct TilePlan {
     int tile;    // 256, 128 or 64
     int splits;
+    int ragged_tail;  // > 0: whole tiles, then this many tail tiles split `splits` ways
 };
 
 TilePlan plan_tiles(const GemmParams& p, const GemmWorkspace& wsp) {
     const int nk1 = p.K1 / BK;
     const double out_bytes = (double)p.M * p.N * 4;
-    TilePlan best{64, 1};
+    // the LayerNorm that follows o or fc2 rides on a uniform split's reduce;
+    // otherwise it is a pass of its own over the fp32 rows (read) and dt rows (write)
+    const double ln_pass = p.ln_out ? (double)p.M * p.N * 6 / 4e12 : 0.0;
+    TilePlan best{64, 1, 0};
     double best_t = 1e30;
     auto consider = [&](int t, double rate) {
         if (p.N % t) return;
         const long tiles = (long)((p.M + t - 1) / t) * (p.N / t);
+        const double t_tile = 2.0 * t * t * p.K1 / rate;
         for (int s = 1; s <= 8; ++s) {
             if (s > 1 && (nk1 / s < PB_GEMM_MIN_KT || !wsp.ws || out_bytes * s > (double)wsp.bytes)) break;
             const long rounds = (tiles * s + 255) / 256;
-            const double k = (double)p.K1 / s;
-            const double tt = rounds * (2.0 * t * t * k / rate) + (s > 1 ? 2.0 * out_bytes * s / 4e12 : 0.0);
+            const double tt = rounds * (t_tile / s) + (s > 1 ? 2.0 * out_bytes * s / 4e12 : ln_pass);
             if (tt < best_t * 0.98) {  // prefer the simpler plan on near ties
                 best_t = tt;
-                best = {t, s};
+                best = {t, s, 0};
+            }
+        }
+        // ragged last round: whole rounds unsplit, the tail tiles split to fill one round
+        const long tail = tiles % 256, full = tiles - tail;
+        if (PB_GEMM_RAGGED && full > 0 && tail > 0 && wsp.ws) {
+            const int s = (int)std::min<long>(8, 256 / tail);
+            const double pbytes = (double)tail * t * t * 4 * s;
+            if (s >= 2 && nk1 / s >= PB_GEMM_MIN_KT && full % 8 == 0 && (tail * s) % 8 == 0 &&
+                pbytes <= (double)wsp.bytes) {
+                const double tt = (full / 256) * t_tile + t_tile / s + 2.0 * pbytes / 4e12 + ln_pass;
+                if (tt < best_t * 0.98) {
+                    best_t = tt;
+                    best = {t, s, (int)tail};
+                }
             }
         }
     };
@@ -484,7 +603,7 @@ TilePlan plan_tiles(const GemmParams& p, const GemmWorkspace& wsp) {
             s = std::min<long>((PB_GEMM_SPLIT_TARGET + tiles - 1) / tiles, std::max(1, nk1 / PB_GEMM_MIN_KT));
             while (s > 1 && out_bytes * s > (double)wsp.bytes) --s;
         }
-        best = {64, std::max(1, s)};
+        best = {64, std::max(1, s), 0};
     }
     return best;
 }
@@ -492,9 +611,11 @@ TilePlan plan_tiles(const GemmParams& p, const GemmWorkspace& wsp) {
 template <typename T, int EPI, int ROLE>
 hipError_t launch_tiles(const GemmParams& p, const GemmWorkspace& wsp, hipStream_t s) {
     const TilePlan tp = plan_tiles(p, wsp);
-    if (tp.tile == 256) return launch_cfg<T, EPI, 256, 256, 2, 4, ROLE, PB_GEMM_S256>(p, wsp, tp.splits, s);
-    if (tp.tile == 128) return launch_cfg<T, EPI, 128, 128, 2, 4, ROLE, PB_GEMM_S128>(p, wsp, tp.splits, s);
-    return launch_cfg<T, EPI, 64, 64, 2, 2, ROLE, PB_GEMM_S64>(p, wsp, tp.splits, s);
+    if (tp.tile == 256)
+        return launch_cfg<T, EPI, 256, 256, 2, 4, ROLE, PB_GEMM_S256>(p, wsp, tp.splits, tp.ragged_tail, s);
+    if (tp.tile == 128)
+        return launch_cfg<T, EPI, 128, 128, 2, 4, ROLE, PB_GEMM_S128>(p, wsp, tp.splits, tp.ragged_tail, s);
+    return launch_cfg<T, EPI, 64, 64, 2, 2, ROLE, PB_GEMM_S64>(p, wsp, tp.splits, tp.ragged_tail, s);
 }
 
 template <typename T>
@@ -511,7 +632,7 @@ hipError_t launch_typed(int role, const GemmParams& p, const GemmWorkspace& wsp,
                 sp = std::min<long>((PB_GEMM_SPLIT_TARGET + tiles - 1) / tiles, std::max(1, p.K1 / BK / PB_GEMM_MIN_KT));
                 while (sp > 1 && (double)p.M * p.N * 4 * sp > (double)wsp.bytes) --sp;
             }
-            return launch_cfg<T, EPI_SHRINK, 64, 64, 2, 2, 4, 4>(p, wsp, std::max(1, sp), s);
+            return launch_cfg<T, EPI_SHRINK, 64, 64, 2, 2, 4, 4>(p, wsp, std::max(1, sp), 0, s);
         }
         default: break;
     }

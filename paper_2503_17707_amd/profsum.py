@@ -73,6 +73,8 @@ def kind_of(name):
         return roles.get(a[5], "gemm")
     if "splitk_resid_ln_kernel" in name:
         return roles[int(re.search(r"splitk_resid_ln_kernelIDF16b?_Li(\d+)E", name).group(1))] + " reduce"
+    if "tail_reduce_kernel" in name:
+        return roles[int(re.search(r"tail_reduce_kernelIDF16b?_Li\d+ELi(\d+)E", name).group(1))] + " reduce"
     if "splitk_reduce_kernel" in name:
         return roles[int(re.search(r"splitk_reduce_kernelIDF16b?_Li\d+ELi(\d+)E", name).group(1))] + " reduce"
     m = re.search(r"gemv_kernelIDF16b?_Li(\d+)E", name)

@@ -47,7 +47,10 @@ DT = {"bf16": 0, "f16": 1}
                                    (1, 2048, 2048), (3, 576, 1600), (8, 128, 8192),
                                    # 256 x 256 tiles: many tiles with a ragged M, and few
                                    # tiles over a long K (split along K)
-                                   (4000, 4096, 512), (2048, 2048, 8192)])
+                                   (4000, 4096, 512), (2048, 2048, 8192),
+                                   # 384 tiles of 256: one whole round, the 128 tail tiles
+                                   # split in two (ragged last round)
+                                   (2048, 12288, 4096)])
 @pytest.mark.parametrize("epi", [0, 1, 2])
 def test_gemm_epilogues(kind, M, N, K, epi):
     import torch
