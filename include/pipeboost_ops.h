@@ -33,6 +33,23 @@ int pb_op_gemm(int32_t dtype, int32_t epi, const void* X, const void* W, const v
                void* C, float* R, int32_t M, int32_t N, int32_t K, float qscale, int32_t qcols,
                void* workspace, size_t workspace_bytes, void* stream);
 
+/* pb_op_gemm with the unmerged LoRA expand folded into the same accumulation
+ * as extra K tiles (Section 2.1: the adapter adds s (x A) B on top of the
+ * fixed W; Section 4.2.2: sequences of one batch may use different adapters):
+ *   Y[m, n] = X[m] . W[n] + Z[m, g zs .. g zs + K2) . W2[n]   if bit g of group_mask
+ *           = X[m] . W[n]                                     otherwise,
+ * with g = n / group (the output group: q, k, v of a fused projection),
+ * then the epilogue of pb_op_gemm.  Z [M, ldz] dt holds each row's scaled
+ * shrink s (x A_slot) in its adapter slot's columns of every group block
+ * (zeros in the other slots' columns, so rows of different adapters, or none,
+ * share the launch); W2 [N, K2] dt holds the B matrices of all slots side by
+ * side.  K2 % 64 == 0, group % 64 == 0; other requirements and the workspace
+ * as pb_op_gemm. */
+int pb_op_gemm_lora(int32_t dtype, int32_t epi, const void* X, const void* W, const void* bias, void* C,
+                    float* R, int32_t M, int32_t N, int32_t K, const void* Z, int32_t ldz, int32_t zs,
+                    const void* W2, int32_t K2, int32_t group, uint32_t group_mask, float qscale,
+                    int32_t qcols, void* workspace, size_t workspace_bytes, void* stream);
+
 /* pb_op_gemm for callers that cannot allocate (code under HIP graph capture,
  * tight serving loops, harnesses that forbid hipMalloc): the same operands,
  * epilogues and kernels, with the split-K partials in a 64 MiB device array

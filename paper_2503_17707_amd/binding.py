@@ -118,6 +118,12 @@ _SIGS = {
                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                                   ctypes.c_int32, ctypes.c_int32, ctypes.c_float, ctypes.c_int32,
                                   ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "pb_op_gemm_lora": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                       ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32,
+                                       ctypes.c_int32, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                       ctypes.c_uint32, ctypes.c_float, ctypes.c_int32, ctypes.c_void_p,
+                                       ctypes.c_size_t, ctypes.c_void_p]),
     "pb_op_gemm_noalloc": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                           ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
@@ -584,6 +590,19 @@ def op_gemm(dtype: int, epi: int, X, W, bias, C=None, R=None, qscale: float = 1.
                            qscale, qcols, _ptr(workspace),
                            0 if workspace is None else workspace.numel() * workspace.element_size(),
                            _stream(stream)))
+
+
+def op_gemm_lora(dtype: int, epi: int, X, W, bias, Z, zs: int, W2, group: int, group_mask: int,
+                 C=None, R=None, qscale: float = 1.0, qcols: int = 0, workspace=None, stream=None):
+    """pb_op_gemm_lora: Z [M, ldz] scaled shrinks (group g's block at column g * zs), W2 [N, K2]."""
+    M, K = X.shape
+    N = W.shape[0]
+    K2 = W2.shape[1]
+    check(lib().pb_op_gemm_lora(dtype, epi, _ptr(X), _ptr(W), _ptr(bias), _ptr(C), _ptr(R), M, N, K,
+                                _ptr(Z), Z.shape[1], zs, _ptr(W2), K2, group, group_mask, qscale, qcols,
+                                _ptr(workspace),
+                                0 if workspace is None else workspace.numel() * workspace.element_size(),
+                                _stream(stream)))
 
 
 def op_gemm_noalloc(dtype: int, epi: int, X, W, bias, C=None, R=None, qscale: float = 1.0,

@@ -1299,9 +1299,17 @@ extern "C" int pb_invalidate_kv(pb_model* m, const uint8_t* layer_lost, int32_t 
 
 namespace {
 
+struct OpLora {
+    const void* Z = nullptr;
+    int32_t ldz = 0, zs = 0;
+    const void* W2 = nullptr;
+    int32_t K2 = 0, group = 0;
+    uint32_t mask = 0;
+};
+
 int op_gemm(int32_t dtype, int32_t epi, const void* X, const void* W, const void* bias, void* C, float* R,
             int32_t M, int32_t N, int32_t K, float qscale, int32_t qcols, const pb::GemmWorkspace& ws,
-            void* stream) {
+            void* stream, const OpLora& lo = OpLora()) {
     if (dtype != PB_BF16 && dtype != PB_F16) return fail(PB_EINVAL, "bad dtype %d", dtype);
     if (epi < 0 || epi > 2) return fail(PB_EINVAL, "epilogue %d not in 0..2", epi);
     if (M < 0 || N <= 0 || K <= 0 || N % 64 || K % 64)
@@ -1310,6 +1318,10 @@ int op_gemm(int32_t dtype, int32_t epi, const void* X, const void* W, const void
     pb::GemmParams p{};
     p.X = X; p.ldx = K; p.W = W; p.ldw = K; p.M = M; p.N = N; p.K1 = K;
     p.bias = bias; p.C = C; p.ldc = N; p.R = R; p.ldr = N; p.qscale = qscale; p.qcols = qcols;
+    if (lo.K2 > 0) {
+        p.X2 = lo.Z; p.ldx2 = lo.ldz; p.x2_group_stride = lo.zs;
+        p.W2 = lo.W2; p.ldw2 = lo.K2; p.K2 = lo.K2; p.group = lo.group; p.k2_mask = lo.mask;
+    }
     const int role = epi == 0 ? 0 : (epi == 1 ? 2 : 3);
     const int e = epi == 0 ? pb::EPI_QKV : (epi == 1 ? pb::EPI_RELU : pb::EPI_RESID);
     HIP_TRY(pb::launch_gemm(dtype, role, e, p, ws, (hipStream_t)stream));
@@ -1323,6 +1335,21 @@ extern "C" int pb_op_gemm(int32_t dtype, int32_t epi, const void* X, const void*
                           int32_t qcols, void* workspace, size_t workspace_bytes, void* stream) {
     const pb::GemmWorkspace ws{workspace, workspace ? workspace_bytes : 0};
     return op_gemm(dtype, epi, X, W, bias, C, R, M, N, K, qscale, qcols, ws, stream);
+}
+
+extern "C" int pb_op_gemm_lora(int32_t dtype, int32_t epi, const void* X, const void* W, const void* bias,
+                               void* C, float* R, int32_t M, int32_t N, int32_t K, const void* Z, int32_t ldz,
+                               int32_t zs, const void* W2, int32_t K2, int32_t group, uint32_t group_mask,
+                               float qscale, int32_t qcols, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+    if (!Z || !W2 || K2 <= 0 || K2 % 64 || group <= 0 || group % 256 || ldz <= 0 || zs < 0)
+        return fail(PB_EINVAL, "pb_op_gemm_lora: bad LoRA operands (K2=%d group=%d ldz=%d zs=%d)", K2, group, ldz, zs);
+    if (N > 0 && group > 0 && (size_t)((N - 1) / group) * zs + K2 > (size_t)ldz)
+        return fail(PB_EINVAL, "pb_op_gemm_lora: group blocks of Z past its row (ldz=%d)", ldz);
+    OpLora lo;
+    lo.Z = Z; lo.ldz = ldz; lo.zs = zs; lo.W2 = W2; lo.K2 = K2; lo.group = group; lo.mask = group_mask;
+    const pb::GemmWorkspace ws{workspace, workspace ? workspace_bytes : 0};
+    return op_gemm(dtype, epi, X, W, bias, C, R, M, N, K, qscale, qcols, ws, stream, lo);
 }
 
 // ---- pb_op_gemm without a caller workspace and without allocating ----------
