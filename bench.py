@@ -295,6 +295,14 @@ def measure(w, steps, warmup, cold_reps, decode_steps, pb, torch, np):
         w.name, (hw.globals_bytes + len(hw.layers) * hw.layer_bytes) / 1e9, hw.pinned_layers,
         len(hw.layers), time.perf_counter() - t0))
     hw_pinned = (hw.pinned_layers, len(hw.layers))
+    try:
+        nodes_online = open("/sys/devices/system/node/online").read().strip()
+    except OSError:
+        nodes_online = "unknown"
+    numa = {"gpu_numa_node": hw.numa_node, "host_nodes_online": nodes_online,
+            "pageable_blobs_bound": sum(1 for b in hw.layers if getattr(b, "bound", False)),
+            "binding": "pinned and pageable host blobs placed on the GPU's NUMA node (preferred policy)"
+                       if hw.numa_node >= 0 else "runtime default placement"}
     t0 = time.perf_counter()
     m = pb.Model(cfg, "cuda:0")
     init_ms = (time.perf_counter() - t0) * 1e3
@@ -457,7 +465,7 @@ def measure(w, steps, warmup, cold_reps, decode_steps, pb, torch, np):
         "tflops": tflops, "ms_step": ms_step, "flops": flops, "ttft": ttft, "loads": loads,
         "b_meas": b_meas, "total_h2d": total_h2d, "bound_ms": bound_ms, "init_ms": init_ms,
         "roofline": roofline, "kernels": kernels, "decode": decode, "merged": merged,
-        "parity": parity, "pinned_layers": hw_pinned[0], "layer_blobs": hw_pinned[1],
+        "parity": parity, "pinned_layers": hw_pinned[0], "layer_blobs": hw_pinned[1], "numa": numa,
     }
 
 
@@ -514,6 +522,9 @@ def main():
                     help="layers of the CPU-oracle sample (0 = all; default: all layers up to "
                          "about 1e13 FLOPs of work, at least one)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-numa", action="store_true",
+                    help="leave host blobs where the runtime and the kernel put them instead of on "
+                         "the GPU's NUMA node")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (3 times) and exit: "
                          "the reference kernel for scaling HBM byte counters")
@@ -535,6 +546,8 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    if args.no_numa:
+        os.environ["PIPEBOOST_NUMA"] = "0"
     import numpy as np
     import torch
 
@@ -641,6 +654,7 @@ def sections(w, r):
                                           "flops_over_warm_rate": ms_step},
                        "ttft_over_max_bound": ttft_med / max(bound_ms, ms_step),
                        "init_ms": r["init_ms"],
+                       "host_numa": r["numa"],
                        "layer_blobs_pinned": r["pinned_layers"],
                        "layer_blobs_staged": staged,
                        "host_memory": ("all layer blobs in pinned host memory" if not staged else

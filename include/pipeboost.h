@@ -124,6 +124,17 @@ size_t pb_arena_bytes(const pb_config* cfg);
 int pb_host_alloc(size_t bytes, void** out);
 int pb_host_free(void* ptr);
 
+/* NUMA node of HIP device `device` (from its PCI address in sysfs), -1 when
+ * the system reports none.  PB_EHIP if the device does not exist. */
+int pb_host_numa_node(int32_t device, int32_t* node);
+
+/* Place later pb_host_alloc allocations (and the loader's pinned staging
+ * ring) on NUMA node `node` (hipHostMallocNumaUser under an MPOL_PREFERRED
+ * policy of the calling thread for the duration of the call), or let the runtime
+ * choose (-1, the default).  Host memory next to the GPU's PCIe root keeps
+ * host-to-device copies off the inter-socket link. */
+int pb_set_host_numa_node(int32_t node);
+
 /* ---- model lifecycle ----------------------------------------------------- */
 
 /* Create a model on the current HIP device over the caller's device arena

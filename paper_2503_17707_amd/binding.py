@@ -62,6 +62,8 @@ _SIGS = {
     "pb_arena_bytes": (ctypes.c_size_t, [ctypes.POINTER(Config)]),
     "pb_host_alloc": (ctypes.c_int, [ctypes.c_size_t, ctypes.POINTER(ctypes.c_void_p)]),
     "pb_host_free": (ctypes.c_int, [ctypes.c_void_p]),
+    "pb_host_numa_node": (ctypes.c_int, [ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]),
+    "pb_set_host_numa_node": (ctypes.c_int, [ctypes.c_int32]),
     "pb_model_create": (ctypes.c_int, [ctypes.POINTER(Config), ctypes.c_void_p, ctypes.c_size_t,
                                        ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.POINTER(ctypes.c_void_p)]),
@@ -229,15 +231,40 @@ class Pinned:
             pass
 
 
-class Pageable:
-    """A page-aligned ordinary (pageable) host buffer with the interface of Pinned."""
+def gpu_numa_node(device: int = 0) -> int:
+    """NUMA node of the GPU (pb_host_numa_node), -1 if the system reports none."""
+    n = ctypes.c_int32(-1)
+    check(lib().pb_host_numa_node(device, ctypes.byref(n)))
+    return n.value
 
-    def __init__(self, nbytes: int):
-        self._buf = np.empty(nbytes + 4096, np.uint8)
+
+def _mbind(ptr: int, nbytes: int, node: int) -> bool:
+    """Prefer one NUMA node for a page-aligned, not yet touched range (mbind,
+    MPOL_PREFERRED), so its pages come from that node whichever thread first
+    writes them (from another node only if that one is full)."""
+    if node < 0 or nbytes <= 0:
+        return False
+    libc = ctypes.CDLL(None, use_errno=True)
+    bits = 8 * ctypes.sizeof(ctypes.c_ulong)
+    mask = (ctypes.c_ulong * (1024 // bits))()
+    mask[node // bits] = 1 << (node % bits)
+    length = (nbytes + 4095) // 4096 * 4096
+    SYS_mbind = 237  # x86_64
+    return libc.syscall(SYS_mbind, ctypes.c_void_p(ptr), ctypes.c_ulong(length), 1, mask,
+                        ctypes.c_ulong(1024), 0) == 0
+
+
+class Pageable:
+    """A page-aligned ordinary (pageable) host buffer with the interface of
+    Pinned; with a NUMA node its pages are bound there before first touch."""
+
+    def __init__(self, nbytes: int, node: int = -1):
+        self._buf = np.empty(nbytes + 2 * 4096, np.uint8)
         off = (-self._buf.ctypes.data) % 4096
         self._arr = self._buf[off:off + nbytes]
         self.ptr = self._arr.ctypes.data
         self.nbytes = nbytes
+        self.bound = _mbind(self.ptr, nbytes, node)
 
     def view(self, dtype=np.uint8) -> np.ndarray:
         return self._arr.view(dtype)
@@ -256,14 +283,20 @@ DEFAULT_PIN_BUDGET = int(float(os.environ.get("PIPEBOOST_PIN_BUDGET_GB", "48")) 
 class HostWeights:
     """Host blobs of a workload in the library's device layout, drawn by synth:
     the globals and LoRA blobs pinned, layer blobs pinned while they fit in
-    pin_budget bytes (in layer-id order) and pageable after that."""
+    pin_budget bytes (in layer-id order) and pageable after that.  With
+    numa (default: on unless PIPEBOOST_NUMA=0) every blob sits on the GPU's
+    NUMA node."""
 
-    def __init__(self, w, cfg: Config, pin_budget: Optional[int] = None):
+    def __init__(self, w, cfg: Config, pin_budget: Optional[int] = None, numa: Optional[bool] = None):
         import synth
 
         self.w, self.cfg = w, cfg
         budget = DEFAULT_PIN_BUDGET if pin_budget is None else pin_budget
         L = lib()
+        if numa is None:
+            numa = os.environ.get("PIPEBOOST_NUMA", "1") != "0"
+        self.numa_node = gpu_numa_node() if numa else -1
+        check(L.pb_set_host_numa_node(self.numa_node))
         kind = w.dtype
         self.layer_bytes = L.pb_layer_bytes(ctypes.byref(cfg))
         self.globals_bytes = L.pb_globals_bytes(ctypes.byref(cfg))
@@ -281,7 +314,7 @@ class HostWeights:
                 blob = Pinned(self.layer_bytes)
                 self.pinned_layers += 1
             else:
-                blob = Pageable(self.layer_bytes)
+                blob = Pageable(self.layer_bytes, self.numa_node)
             self._zero_padding(blob, cfg)
             for name in synth.LAYER_TENSORS:
                 off, _ = layer_tensor(cfg, name)

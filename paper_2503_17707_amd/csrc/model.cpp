@@ -16,16 +16,21 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cctype>
 #include <chrono>
 #include <condition_variable>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <atomic>
 #include <mutex>
 #include <string>
 #include <thread>
 #include <vector>
+
+#include <sys/syscall.h>
+#include <unistd.h>
 
 #include "../../include/pipeboost.h"
 #include "kernels.h"
@@ -386,10 +391,62 @@ size_t pb_arena_bytes(const pb_config* cfg) {
     return arena_layout(cfg).total;
 }
 
+namespace {
+
+// NUMA node that pinned allocations are placed on (-1: the runtime's choice)
+std::atomic<int> g_host_node{-1};
+
+// MPOL_PREFERRED of one node for the calling thread while it lives, so that
+// hipHostMalloc with hipHostMallocNumaUser takes its pages there (other
+// nodes only if that one is full); the default policy is restored afterwards
+struct BindThreadToNode {
+    bool active = false;
+    explicit BindThreadToNode(int node) {
+        if (node < 0 || node >= 1024) return;
+        unsigned long mask[1024 / (8 * sizeof(unsigned long))] = {};
+        mask[node / (8 * sizeof(unsigned long))] = 1UL << (node % (8 * sizeof(unsigned long)));
+        active = syscall(SYS_set_mempolicy, 1 /* MPOL_PREFERRED */, mask, (unsigned long)1024) == 0;
+    }
+    ~BindThreadToNode() {
+        if (active) (void)syscall(SYS_set_mempolicy, 0 /* MPOL_DEFAULT */, nullptr, 0UL);
+    }
+};
+
+hipError_t host_malloc_on_node(void** out, size_t bytes) {
+    const int node = g_host_node.load();
+    if (node < 0) return hipHostMalloc(out, bytes, hipHostMallocDefault);
+    BindThreadToNode bind(node);
+    return hipHostMalloc(out, bytes, bind.active ? hipHostMallocNumaUser : hipHostMallocDefault);
+}
+
+}  // namespace
+
+int pb_host_numa_node(int32_t device, int32_t* node) {
+    if (!node) return fail(PB_EINVAL, "pb_host_numa_node: node is NULL");
+    *node = -1;
+    char bus[64] = {};
+    HIP_TRY(hipDeviceGetPCIBusId(bus, (int)sizeof(bus) - 1, device));
+    for (char* c = bus; *c; ++c) *c = (char)std::tolower((unsigned char)*c);
+    const std::string path = std::string("/sys/bus/pci/devices/") + bus + "/numa_node";
+    FILE* f = std::fopen(path.c_str(), "r");
+    if (!f) return PB_OK;  // no NUMA information: -1
+    int v = -1;
+    if (std::fscanf(f, "%d", &v) != 1) v = -1;
+    std::fclose(f);
+    *node = v;
+    return PB_OK;
+}
+
+int pb_set_host_numa_node(int32_t node) {
+    if (node < -1 || node >= 1024) return fail(PB_EINVAL, "pb_set_host_numa_node: node %d out of range", node);
+    g_host_node.store(node);
+    return PB_OK;
+}
+
 int pb_host_alloc(size_t bytes, void** out) {
     if (!out || bytes == 0) return fail(PB_EINVAL, "pb_host_alloc: bad arguments");
     *out = nullptr;
-    hipError_t e = hipHostMalloc(out, bytes, hipHostMallocDefault);
+    hipError_t e = host_malloc_on_node(out, bytes);
     if (e != hipSuccess) {
         *out = nullptr;
         return fail(PB_ENOMEM, "hipHostMalloc(%zu) failed: %s", bytes, hipGetErrorString(e));
@@ -611,7 +668,7 @@ int pb_stream_layers(pb_model* m, const int32_t* layer_order, int32_t n_layers,
     const bool all_pinned = std::all_of(jobs.begin(), jobs.end(), [](const LoadJob& j) { return j.pinned; });
     if (!all_pinned && !m->ring[0]) {
         for (int k = 0; k < STAGE_SLOTS; ++k) {
-            if (hipHostMalloc((void**)&m->ring[k], STAGE_BYTES, 0) != hipSuccess)
+            if (host_malloc_on_node((void**)&m->ring[k], STAGE_BYTES) != hipSuccess)
                 return fail(PB_ENOMEM, "pinned staging ring allocation failed");
             HIP_TRY(hipEventCreateWithFlags(&m->ring_ev[k], hipEventDisableTiming));
         }

@@ -83,3 +83,17 @@ def test_invalid_configs_are_refused():
         off = ctypes.c_size_t()
         assert L.pb_layer_tensor(ctypes.byref(cfg), 0, ctypes.byref(off), None) == pb.PB_EINVAL
         assert L.pb_last_error().decode()
+
+
+def test_pageable_blob_binds_to_a_numa_node_before_first_touch():
+    import numpy as np
+
+    from paper_2503_17707_amd import binding as pb
+
+    b = pb.Pageable(3 << 20, 0)  # node 0 exists on every Linux host
+    assert b.bound
+    assert b.ptr % 4096 == 0
+    v = b.view()
+    v[:] = 5
+    assert int(v.sum()) == 5 * (3 << 20)
+    assert not pb.Pageable(1 << 20, -1).bound
