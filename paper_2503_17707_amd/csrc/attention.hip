@@ -38,6 +38,9 @@ namespace {
 #ifndef PB_ATTN_KS2
 #define PB_ATTN_KS2 1  // allow two wave groups splitting the keys
 #endif
+#ifndef PB_ATTN_MFMA_SUM
+#define PB_ATTN_MFMA_SUM 1  // softmax row sums by the matrix unit (a tile of ones in P V)
+#endif
 #ifndef PB_ATTN_KSWZ16
 #define PB_ATTN_KSWZ16 1  // K tiles of head_dim 128 permuted over all 16 chunks
 #endif
@@ -46,6 +49,11 @@ namespace {
 #endif
 
 constexpr float LOG2E = 1.4426950408889634f;
+
+// two 1.0 values of dt packed in 32 bits
+template <typename T> __device__ constexpr uint32_t ONE2();
+template <> __device__ constexpr uint32_t ONE2<_Float16>() { return 0x3C003C00u; }
+template <> __device__ constexpr uint32_t ONE2<__bf16>() { return 0x3F803F80u; }
 constexpr int BKV = 64;  // keys per tile
 
 // 16-byte chunk permutations of a K or V tile row (key = row): K is read as
@@ -164,29 +172,47 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
     // then V; lane i fills row RPI * (I' % (NIG / 2)) + i / CPR (I' = I % NIG),
     // physical chunk i % CPR, i.e. logical chunk (i % CPR) ^ permutation of
     // that row.  Tiles past the last one re-read its key rows (not used).
+    // Per-lane parts of each slot's source (row within the tile, byte offset
+    // of its chunk within a K or V row) are fixed; a tile only moves the key.
+    // Offsets are 32-bit bytes from the wave-uniform base of this (sequence,
+    // head) (the launcher checks they fit).
     const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
+    const T* kvbase = kvsrc + b * kv_seq + h * HD;
+    const uint32_t ldb = (uint32_t)kv_ld * 2;
+    int srow[NL];
+    uint32_t scol[NL];
+#pragma unroll
+    for (int j = 0; j < NL; ++j) {
+        const int I = wave + NW * j, Ig = I % NIG;
+        const bool isv = Ig >= NIG / 2;
+        srow[j] = RPI * (Ig % (NIG / 2)) + lane / CPR;
+        const int pch = lane % CPR;
+        const int ch = isv ? vswz<HD>(srow[j], pch) : kswz<HD>(srow[j], pch);
+        scol[j] = (uint32_t)((isv ? d : 0) + ch * 8) * 2;
+    }
     auto issue = [&](int it, int stage) {
         const uint32_t sbase = lds0 + stage * STAGE;
 #pragma unroll
         for (int j = 0; j < NL; ++j) {
             const int I = wave + NW * j;
-            const int kb = it * KS + I / NIG, Ig = I % NIG;
-            const bool isv = Ig >= NIG / 2;
-            const int row = RPI * (Ig % (NIG / 2)) + lane / CPR;
-            const int pch = lane % CPR;
-            const int ch = isv ? vswz<HD>(row, pch) : kswz<HD>(row, pch);
-            const int key = min(kb * BKV + row, T_len - 1);
-            const T* src = kvsrc + b * kv_seq + key * kv_ld + (isv ? d : 0) + h * HD + ch * 8;
-            dma16(src, sbase + (uint32_t)__builtin_amdgcn_readfirstlane(I * 1024));
+            const int kb = it * KS + I / NIG;
+            const int key = min(kb * BKV + srow[j], T_len - 1);
+            dma16s(kvbase, (uint32_t)key * ldb + scol[j],
+                   sbase + (uint32_t)__builtin_amdgcn_readfirstlane(I * 1024));
         }
     };
 
     f32x4 o[NQG][CT];
     float m_run[NQG], l_run[NQG];
+    // running sums by the matrix unit: one more O^T tile, ones^T P^T, every
+    // row of which is the sum of the query's probabilities as they enter the
+    // products (rounded to dt), rescaled with O
+    f32x4 o_l[NQG];
 #pragma unroll
     for (int qg = 0; qg < NQG; ++qg) {
         m_run[qg] = -INFINITY;
         l_run[qg] = 0.f;
+        o_l[qg] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) o[qg][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
@@ -256,10 +282,12 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
                 for (int r = 0; r < 4; ++r) {
                     const float e = __builtin_amdgcn_exp2f(sc[qg][jt][r] * LOG2E - mb);
                     pt[jt][r] = (T)e;
-                    psum += e;
+                    if (!PB_ATTN_MFMA_SUM) psum += e;
                 }
-            psum = group4_sum(psum);
-            l_run[qg] = l_run[qg] * alpha + psum;
+            if (!PB_ATTN_MFMA_SUM) {
+                psum = group4_sum(psum);
+                l_run[qg] = l_run[qg] * alpha + psum;
+            }
             m_run[qg] = m_new;
             if (__any(alpha != 1.f)) {
 #pragma unroll
@@ -268,6 +296,12 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
                     o[qg][ct][1] *= alpha;
                     o[qg][ct][2] *= alpha;
                     o[qg][ct][3] *= alpha;
+                }
+                if (PB_ATTN_MFMA_SUM) {
+                    o_l[qg][0] *= alpha;
+                    o_l[qg][1] *= alpha;
+                    o_l[qg][2] *= alpha;
+                    o_l[qg][3] *= alpha;
                 }
             }
             // P^T operand of key step ks: k index 8 lg + 4 hh + r <-> key 32 ks + 16 hh + 4 lg + r
@@ -304,6 +338,11 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
 #pragma unroll
                 for (int qg = 0; qg < NQG; ++qg) o[qg][ct] = Mfma<T>::mma(vf, pf[qg][ks], o[qg][ct]);
             }
+            if (PB_ATTN_MFMA_SUM) {
+                const vec8 ones = as_vec8<T>(u32x4{ONE2<T>(), ONE2<T>(), ONE2<T>(), ONE2<T>()});
+#pragma unroll
+                for (int qg = 0; qg < NQG; ++qg) o_l[qg] = Mfma<T>::mma(ones, pf[qg][ks], o_l[qg]);
+            }
         }
     };
     // S-stage ring: iterations it+1 .. it+S-2 are in flight while it is used
@@ -323,6 +362,10 @@ void attention_kernel(const T* __restrict__ qkv, const T* __restrict__ kvsrc, in
         body(it);
     }
 
+    if (PB_ATTN_MFMA_SUM) {
+#pragma unroll
+        for (int qg = 0; qg < NQG; ++qg) l_run[qg] = o_l[qg][0];
+    }
     if (KS == 2) {
         // merge group 1's (max, sum, O^T) into group 0's: every lane holds
         // the same query and O^T rows in both groups
@@ -531,6 +574,8 @@ hipError_t launch_attention_kv(int dtype, const void* qkv, const void* kv, int64
     if (B <= 0 || T_len <= 0) return hipSuccess;
     if ((int64_t)B * T_len * 3 * H * hd >= ((int64_t)1 << 31) || (int64_t)B * kv_seq >= ((int64_t)1 << 31))
         return hipErrorInvalidValue;
+    // copy offsets are 32-bit bytes within one (sequence, head)
+    if (((int64_t)T_len * kv_ld + 3 * (int64_t)H * hd) * 2 >= ((int64_t)1 << 32)) return hipErrorInvalidValue;
     if (dtype == 1) {
         if (hd == 64) return launch_qw<_Float16, 64>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);
         if (hd == 128) return launch_qw<_Float16, 128>(qkv, kv, kv_ld, kv_seq, out, B, T_len, H, s);

@@ -61,6 +61,22 @@ __device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
         : "memory");
 }
 
+// The same copy with a wave-uniform 64-bit base (SGPRs) and a 32-bit
+// per-lane byte offset (global_load_lds_dwordx4 voffset, saddr): the base
+// stays scalar and each lane's address costs one 32-bit offset.
+__device__ __forceinline__ void dma16s(const void* sbase, uint32_t voff, uint32_t lds_base) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %2, %3\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds_base), "v"(voff), "s"(sbase)
+        : "memory");
+}
+
 // s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
