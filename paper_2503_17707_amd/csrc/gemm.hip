@@ -284,20 +284,32 @@ void gemm_kernel(GemmParams p, SplitArgs sa) {
     const T* Wb = (const T*)p.W;
     const T* W2 = (const T*)p.W2;
     const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
+    // each slot's row is the same in every K tile: its byte offset (row and
+    // chunk) is taken once, a tile adds its K offset to it; the operand bases
+    // stay in scalar registers (byte offsets fit in 32 bits: the launcher
+    // keeps rows * leading dimension below 2^31 elements)
+    uint32_t soff[NL];
+#pragma unroll
+    for (int j = 0; j < NL; ++j)
+        soff[j] = j < NLX ? ((uint32_t)min(xr0 + 8 * NW * j, p.M - 1) * (uint32_t)p.ldx + chk) * 2
+                          : ((uint32_t)min(wr0 + 8 * NW * j, p.N - 1) * (uint32_t)p.ldw + chk) * 2;
     auto issue = [&](int t, int stage) {
         const uint32_t sbase = lds0 + stage * STAGE;
-        const bool base = t < nk1;
-        const T* xp = base ? Xb : X2;
-        const T* wp = base ? Wb : W2;
-        const int ldx = base ? (int)p.ldx : (int)p.ldx2;
-        const int ldw = base ? (int)p.ldw : (int)p.ldw2;
-        const int k = (base ? t : t - nk1) * BK + chk;
+        if (t < nk1) {
+            const uint32_t kb = (uint32_t)t * BK * 2;
 #pragma unroll
-        for (int j = 0; j < NL; ++j) {
-            const int off = j < NLX ? min(xr0 + 8 * NW * j, p.M - 1) * ldx + k
-                                    : min(wr0 + 8 * NW * j, p.N - 1) * ldw + k;
-            dma16((j < NLX ? xp : wp) + off,
-                  sbase + (uint32_t)__builtin_amdgcn_readfirstlane((wave + NW * j) * 1024));
+            for (int j = 0; j < NL; ++j)
+                dma16s(j < NLX ? (const void*)Xb : (const void*)Wb, soff[j] + kb,
+                       sbase + (uint32_t)__builtin_amdgcn_readfirstlane((wave + NW * j) * 1024));
+        } else {  // LoRA K tiles: [Z | B] rows of the same slots
+            const int k = (t - nk1) * BK + chk;
+#pragma unroll
+            for (int j = 0; j < NL; ++j) {
+                const int off = j < NLX ? min(xr0 + 8 * NW * j, p.M - 1) * (int)p.ldx2 + k
+                                        : min(wr0 + 8 * NW * j, p.N - 1) * (int)p.ldw2 + k;
+                dma16((j < NLX ? X2 : W2) + off,
+                      sbase + (uint32_t)__builtin_amdgcn_readfirstlane((wave + NW * j) * 1024));
+            }
         }
     };
 
