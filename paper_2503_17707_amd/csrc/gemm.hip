@@ -60,6 +60,9 @@ namespace {
 #ifndef PB_GEMV_KW8
 #define PB_GEMV_KW8 1  // GEMV rows of K >= 4096 split over eight waves
 #endif
+#ifndef PB_GEMV_NT
+#define PB_GEMV_NT 1  // weights streamed by the GEMV with non-temporal loads
+#endif
 #ifndef PB_GEMV_RPB
 #define PB_GEMV_RPB 4  // output features per GEMV block
 #endif
@@ -672,7 +675,14 @@ __device__ __forceinline__ void gemv_dot(const T* __restrict__ X, int64_t ldx, c
         for (int u = 0; u < 2; ++u) {
             const int c = min(c0 + u * 512, ke - 8);  // in bounds; the excess is not accumulated
 #pragma unroll
-            for (int r = 0; r < RPB; ++r) wr[u][r] = *(const u32x4*)(W + (int64_t)(n0 + r) * ldw + c);
+            for (int r = 0; r < RPB; ++r) {
+                const u32x4* src = (const u32x4*)(W + (int64_t)(n0 + r) * ldw + c);
+#if PB_GEMV_NT
+                wr[u][r] = __builtin_nontemporal_load(src);  // each weight is read once per step
+#else
+                wr[u][r] = *src;
+#endif
+            }
 #pragma unroll
             for (int m = 0; m < MR; ++m) xr[u][m] = *(const u32x4*)(X + (int64_t)min(m, M - 1) * ldx + c);
         }

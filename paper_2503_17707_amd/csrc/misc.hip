@@ -76,6 +76,9 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict_
 // vocabulary rows at a time (lanes split the model width into 16-byte chunks),
 // and each block also writes, per sequence, the (max, lowest index) of the
 // rows it covered, so the final argmax only scans one partial per block.
+#ifndef PB_LM_NT
+#define PB_LM_NT 1  // embedding rows read with non-temporal loads (44.1 -> 38.6 us at OPT-1.3B)
+#endif
 constexpr int LM_ROWS = 8;                      // rows per wave pass
 constexpr int LM_BLOCK_ROWS = 4 * 2 * LM_ROWS;  // 4 waves x 2 passes
 
@@ -110,8 +113,14 @@ __global__ __launch_bounds__(256) void lm_head_kernel(const float* __restrict__ 
         for (int c = lane * 8; c < d; c += 64 * 8) {
             u32x4 ev[LM_ROWS];
 #pragma unroll
-            for (int r = 0; r < LM_ROWS; ++r)
-                ev[r] = *(const u32x4*)(E + (int64_t)min(v0 + r, V - 1) * d + c);
+            for (int r = 0; r < LM_ROWS; ++r) {
+                const u32x4* src = (const u32x4*)(E + (int64_t)min(v0 + r, V - 1) * d + c);
+#if PB_LM_NT
+                ev[r] = __builtin_nontemporal_load(src);  // streamed once: no reuse to keep in cache
+#else
+                ev[r] = *src;
+#endif
+            }
             float zb[NB][8];
 #pragma unroll
             for (int j = 0; j < NB; ++j) {
