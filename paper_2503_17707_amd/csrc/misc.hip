@@ -63,11 +63,13 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict_
             s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
         }
     }
+    // with gridDim.y > 1 every block of the row normalizes it, block 0 writes
+    // it, and the blocks share the row's LoRA shrink
     void* orow = OUT_F32 ? (void*)((float*)out + (int64_t)row * d) : (void*)((T*)out + (int64_t)row * d);
-    row_layernorm<T, MAXC, OUT_F32>(v, s, nc, g, b, orow, eps, red);
+    row_layernorm<T, MAXC, OUT_F32>(v, s, nc, g, b, blockIdx.y == 0 ? orow : nullptr, eps, red);
     if (!OUT_F32 && sh.Acat) {
         __shared__ float red16[4][16];
-        row_shrink<T, MAXC>(sh, row, d, v, red16);
+        row_shrink<T, MAXC>(sh, row, d, v, red16, (int)blockIdx.y, (int)gridDim.y);
     }
 }
 
@@ -310,8 +312,13 @@ hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t i
     if (d % 4 || d > 256 * 4 * LN_MAXC) return hipErrorInvalidValue;
     RowShrink sh{};
     if (shp && !out_f32) sh = *shp;
+    // a few rows (decode steps): the row's shrink groups of 16 ranks go to
+    // blocks of their own, so that the A reads spread over several CUs
+    int slices = 1;
+    if (sh.Acat && rows <= 8)
+        slices = std::max(1, __builtin_popcount(sh.mask & 7u) * ((sh.rs + 15) / 16));
 #define PB_LN1(T, F, C)                                                                            \
-    PB_LAUNCH((layernorm_kernel<T, F, C>), dim3(rows), dim3(256), 0, s, x, in_mul, in_add, \
+    PB_LAUNCH((layernorm_kernel<T, F, C>), dim3(rows, slices), dim3(256), 0, s, x, in_mul, in_add, \
                        (const T*)g, (const T*)b, out, d, eps, sh)
 #define PB_LN(T, F)                                                                                \
     do {                                                                                           \

@@ -883,11 +883,11 @@ int enqueue_forward(pb_model* m, int B, int T, bool use_lora, uint32_t lora_unio
     }
     const bool qkv_lora = use_lora && (lora_union & (PB_LORA_Q | PB_LORA_K | PB_LORA_V));
     const bool o_lora = use_lora && (lora_union & PB_LORA_O);
-    // For few tokens the q/k/v LoRA shrink rides on the kernel that writes the
-    // LayerNorm rows (row-wise dot products); for many it is a GEMM, and for a
-    // handful (decode steps) a GEMV, whose blocks share the A reads that one
-    // LayerNorm block per row would make alone.
-    const bool fuse_shrink = qkv_lora && N > pb::GEMV_MAX_ROWS && N <= ROW_SHRINK_MAX_TOKENS;
+    // Up to 1024 tokens the q/k/v LoRA shrink rides on the kernel that writes
+    // the LayerNorm rows (row-wise dot products; for a handful of rows, decode
+    // steps, each row's 16-rank groups go to blocks of their own so that the A
+    // reads spread over several CUs); for more tokens it is a GEMM.
+    const bool fuse_shrink = qkv_lora && N <= ROW_SHRINK_MAX_TOKENS;
     auto row_shrink_args = [&](int layer) {
         pb::RowShrink sh{};
         if (fuse_shrink) {

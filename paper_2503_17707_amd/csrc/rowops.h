@@ -36,6 +36,7 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
 // (biased variance), written as dt, or fp32 when OUT_F32.  g and b are loaded
 // before the reductions so that their latency hides behind them.  For dt
 // output v is left holding the values rounded to dt, as the next GEMM reads them.
+// out_row NULL: nothing is written (v is still updated).
 template <typename T, int MAXC, bool OUT_F32>
 __device__ __forceinline__ void row_layernorm(f32x4 (&v)[MAXC], float sum, int nc, const T* g, const T* b,
                                               void* out_row, float eps, float* red) {
@@ -73,9 +74,9 @@ __device__ __forceinline__ void row_layernorm(f32x4 (&v)[MAXC], float sum, int n
 #pragma unroll
             for (int r = 0; r < 4; ++r) y[r] = (v[i][r] - mean) * rstd * (float)ga[r] + (float)ba[r];
             if (OUT_F32) {
-                *(f32x4*)((float*)out_row + 4 * c) = f32x4{y[0], y[1], y[2], y[3]};
+                if (out_row) *(f32x4*)((float*)out_row + 4 * c) = f32x4{y[0], y[1], y[2], y[3]};
             } else {
-                *(u32x2*)((T*)out_row + 4 * c) = pack4<T>(y[0], y[1], y[2], y[3]);
+                if (out_row) *(u32x2*)((T*)out_row + 4 * c) = pack4<T>(y[0], y[1], y[2], y[3]);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) v[i][r] = (float)(T)y[r];
             }
@@ -115,26 +116,33 @@ __device__ __forceinline__ float wave_sum16(const float (&p)[16], int lane) {
 // threads of the block (it synchronizes).  The loads of a chunk's 16 A rows
 // are unconditional (ranks past rs re-read row rs - 1 and are dropped) so that
 // they are in flight together.
+//
+// With several blocks per row (slice of nslice), block `slice` takes every
+// nslice-th group of 16 ranks (targets in order) and only slice 0 writes the
+// zero columns.
 template <typename T, int MAXC>
 __device__ __forceinline__ void row_shrink(const RowShrink& sh, int m, int d, const f32x4 (&u)[MAXC],
-                                           float (*red)[16]) {
+                                           float (*red)[16], int slice = 0, int nslice = 1) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int nc = d / 4;
     const int slot = sh.row_slot[m];
     T* zr = (T*)sh.Z + (int64_t)m * 4 * sh.kw;
     // zero every column outside the row's own slot block of an active target
-    for (int c = tid; c < 3 * sh.kw; c += 256) {
-        const int t = c / sh.kw, cc = c % sh.kw;
-        const bool own = slot >= 0 && ((sh.mask >> t) & 1u) && cc >= slot * sh.rs && cc < (slot + 1) * sh.rs;
-        if (!own) zr[c] = (T)0.f;
-    }
+    if (slice == 0)
+        for (int c = tid; c < 3 * sh.kw; c += 256) {
+            const int t = c / sh.kw, cc = c % sh.kw;
+            const bool own = slot >= 0 && ((sh.mask >> t) & 1u) && cc >= slot * sh.rs && cc < (slot + 1) * sh.rs;
+            if (!own) zr[c] = (T)0.f;
+        }
     if (slot < 0) return;  // uniform across the block
     const float scale = sh.slot_scale[slot];
     const T* A = (const T*)sh.Acat;
     const int o_lane = 8 * ((lane >> 5) & 1) + 4 * ((lane >> 4) & 1) + 2 * ((lane >> 3) & 1) + ((lane >> 2) & 1);
+    int group = 0;
     for (int t = 0; t < 3; ++t) {
         if (!((sh.mask >> t) & 1u)) continue;
         for (int j0 = 0; j0 < sh.rs; j0 += 16) {
+            if (group++ % nslice != slice) continue;  // uniform across the block
             const T* rows[16];
 #pragma unroll
             for (int o = 0; o < 16; ++o)
