@@ -513,7 +513,7 @@ def main():
                          "fits one GPU)")
     ap.add_argument("--extra-workload", default="opt-1.3b",
                     help="a second, smaller workload measured first and reported under "
-                         "'extra' ('' = none)")
+                         "'extra' ('' or 'none' = none)")
     ap.add_argument("--cold-reps", type=int, default=5)
     ap.add_argument("--layers", type=int, default=0,
                     help="run only the first N layers of the headline workload's shape (for "
@@ -578,7 +578,7 @@ def main():
         print(json.dumps(gemm_reference(w, pb, torch)), flush=True)
         return
     out_extra = None
-    if args.extra_workload and args.extra_workload != args.workload:
+    if args.extra_workload and args.extra_workload not in ("none", args.workload):
         we = synth.WORKLOADS[args.extra_workload]
         r = measure(we, max(args.steps, 50), args.warmup, args.cold_reps, args.decode_steps,
                     pb, torch, np)

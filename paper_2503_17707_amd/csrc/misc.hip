@@ -43,7 +43,9 @@ __global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ 
 // ---- LayerNorm: one 256-thread block per row, values kept in registers ------
 constexpr int LN_MAXC = 16;  // float4 chunks per thread: d <= 256 * 4 * 16
 
-template <typename T, bool OUT_F32, int MAXC>
+// SHRINK: the row's LoRA shrink rides along (compiled only where it is used,
+// since its registers would lower the occupancy of the plain kernel)
+template <typename T, bool OUT_F32, int MAXC, bool SHRINK>
 __global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict__ x,
                                                        int64_t in_mul, int64_t in_add,
                                                        const T* __restrict__ g,
@@ -67,7 +69,7 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict_
     // it, and the blocks share the row's LoRA shrink
     void* orow = OUT_F32 ? (void*)((float*)out + (int64_t)row * d) : (void*)((T*)out + (int64_t)row * d);
     row_layernorm<T, MAXC, OUT_F32>(v, s, nc, g, b, blockIdx.y == 0 ? orow : nullptr, eps, red);
-    if (!OUT_F32 && sh.Acat) {
+    if (!OUT_F32 && SHRINK) {
         __shared__ float red16[4][16];
         row_shrink<T, MAXC>(sh, row, d, v, red16, (int)blockIdx.y, (int)gridDim.y);
     }
@@ -317,14 +319,24 @@ hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t i
     int slices = 1;
     if (sh.Acat && rows <= 8)
         slices = std::max(1, __builtin_popcount(sh.mask & 7u) * ((sh.rs + 15) / 16));
+#define PB_LN2(T, F, C, SH)                                                                        \
+    PB_LAUNCH((layernorm_kernel<T, F, C, SH>), dim3(rows, slices), dim3(256), 0, s, x, in_mul,      \
+              in_add, (const T*)g, (const T*)b, out, d, eps, sh)
 #define PB_LN1(T, F, C)                                                                            \
-    PB_LAUNCH((layernorm_kernel<T, F, C>), dim3(rows, slices), dim3(256), 0, s, x, in_mul, in_add, \
-                       (const T*)g, (const T*)b, out, d, eps, sh)
+    do {                                                                                           \
+        if (!F && sh.Acat) PB_LN2(T, false, C, true);                                              \
+        else PB_LN2(T, F, C, false);                                                               \
+    } while (0)
+    // chunks per thread fitted to d: registers decide how many rows a CU
+    // keeps in flight, and the kernel is bound by the latency of its rows
 #define PB_LN(T, F)                                                                                \
     do {                                                                                           \
         if (d <= 2048) PB_LN1(T, F, 2);                                                            \
         else if (d <= 4096) PB_LN1(T, F, 4);                                                       \
+        else if (d <= 5120) PB_LN1(T, F, 5);                                                       \
         else if (d <= 8192) PB_LN1(T, F, 8);                                                       \
+        else if (d <= 9216) PB_LN1(T, F, 9);                                                       \
+        else if (d <= 12288) PB_LN1(T, F, 12);                                                     \
         else PB_LN1(T, F, LN_MAXC);                                                                \
     } while (0)
     if (dtype == 1) {
@@ -334,6 +346,7 @@ hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t i
     }
 #undef PB_LN
 #undef PB_LN1
+#undef PB_LN2
     return hipGetLastError();
 }
 

@@ -33,21 +33,26 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
 // LayerNorm of one row of d = 4 nc values held by the 256 threads of a block
 // as float4 chunks (chunk i of a thread = columns 4 (tid + 256 i) .. +3; sum =
 // this thread's sum of its values): out = LN(v) * g + b with fp32 statistics
-// (biased variance), written as dt, or fp32 when OUT_F32.  g and b are loaded
-// before the reductions so that their latency hides behind them.  For dt
+// (biased variance), written as dt, or fp32 when OUT_F32.  For dt
 // output v is left holding the values rounded to dt, as the next GEMM reads them.
 // out_row NULL: nothing is written (v is still updated).
 template <typename T, int MAXC, bool OUT_F32>
 __device__ __forceinline__ void row_layernorm(f32x4 (&v)[MAXC], float sum, int nc, const T* g, const T* b,
                                               void* out_row, float eps, float* red) {
     const int tid = threadIdx.x;
-    u32x2 graw[MAXC], braw[MAXC];
+    // narrow rows: g and b preloaded (their latency hides behind the
+    // reductions); wide rows: loaded at the end, their registers would cost
+    // rows in flight
+    constexpr bool PRE = MAXC <= 4;
+    u32x2 graw[PRE ? MAXC : 1], braw[PRE ? MAXC : 1];
+    if (PRE) {
 #pragma unroll
-    for (int i = 0; i < MAXC; ++i) {
-        const int c = tid + 256 * i;
-        if (c < nc) {
-            graw[i] = *(const u32x2*)(g + 4 * c);
-            braw[i] = *(const u32x2*)(b + 4 * c);
+        for (int i = 0; i < MAXC; ++i) {
+            const int c = tid + 256 * i;
+            if (c < nc) {
+                graw[PRE ? i : 0] = *(const u32x2*)(g + 4 * c);
+                braw[PRE ? i : 0] = *(const u32x2*)(b + 4 * c);
+            }
         }
     }
     const float inv_d = 1.0f / (float)(4 * nc);
@@ -68,8 +73,10 @@ __device__ __forceinline__ void row_layernorm(f32x4 (&v)[MAXC], float sum, int n
         const int c = tid + 256 * i;
         if (c < nc) {
             T ga[4], ba[4];
-            __builtin_memcpy(ga, &graw[i], 8);
-            __builtin_memcpy(ba, &braw[i], 8);
+            const u32x2 gr = PRE ? graw[PRE ? i : 0] : *(const u32x2*)(g + 4 * c);
+            const u32x2 br = PRE ? braw[PRE ? i : 0] : *(const u32x2*)(b + 4 * c);
+            __builtin_memcpy(ga, &gr, 8);
+            __builtin_memcpy(ba, &br, 8);
             float y[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) y[r] = (v[i][r] - mean) * rstd * (float)ga[r] + (float)ba[r];
