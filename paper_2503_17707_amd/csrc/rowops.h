@@ -20,6 +20,24 @@ struct RowShrink {
     uint32_t mask;           // targets q=1, k=2, v=4
 };
 
+// One LayerNorm output before rounding: (v - mean) rstd g + b, with the
+// rounding steps spelled out (product, then one fused multiply-add) so that
+// every kernel that normalizes a row gets the same bits, whatever the
+// compiler would contract.  The empty asm keeps the result an fp32 value:
+// otherwise a later conversion to fp16 may be folded into a mixed-precision
+// multiply-add that rounds once to fp16 instead of to fp32 and then to fp16.
+__device__ __forceinline__ float ln_apply(float v, float mean, float rstd, float g, float b) {
+    float y = __builtin_fmaf((v - mean) * rstd, g, b);
+    asm("" : "+v"(y));
+    return y;
+}
+
+// 1 / sqrt(var + eps) from the block sum of squared deviations, the variance
+// rounded inside one fused multiply-add (q inv_d + eps)
+__device__ __forceinline__ float ln_rstd(float qsum, float inv_d, float eps) {
+    return 1.0f / sqrtf(__builtin_fmaf(qsum, inv_d, eps));
+}
+
 // Sum over the 256 threads of a block (4 waves); red holds 4 floats.
 __device__ __forceinline__ float block_sum256(float v, float* red) {
     v = wave_sum(v);
@@ -39,6 +57,7 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
 template <typename T, int MAXC, bool OUT_F32>
 __device__ __forceinline__ void row_layernorm(f32x4 (&v)[MAXC], float sum, int nc, const T* g, const T* b,
                                               void* out_row, float eps, float* red) {
+#pragma clang fp contract(off)  // only the fused multiply-adds written out below
     const int tid = threadIdx.x;
     // narrow rows: g and b preloaded (their latency hides behind the
     // reductions); wide rows: loaded at the end, their registers would cost
@@ -64,10 +83,9 @@ __device__ __forceinline__ void row_layernorm(f32x4 (&v)[MAXC], float sum, int n
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const float t = v[i][r] - mean;
-                q += t * t;
+                q = __builtin_fmaf(t, t, q);
             }
-    const float var = block_sum256(q, red) * inv_d;
-    const float rstd = 1.0f / sqrtf(var + eps);
+    const float rstd = ln_rstd(block_sum256(q, red), inv_d, eps);
 #pragma unroll
     for (int i = 0; i < MAXC; ++i) {
         const int c = tid + 256 * i;
@@ -79,7 +97,7 @@ __device__ __forceinline__ void row_layernorm(f32x4 (&v)[MAXC], float sum, int n
             __builtin_memcpy(ba, &br, 8);
             float y[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) y[r] = (v[i][r] - mean) * rstd * (float)ga[r] + (float)ba[r];
+            for (int r = 0; r < 4; ++r) y[r] = ln_apply(v[i][r], mean, rstd, (float)ga[r], (float)ba[r]);
             if (OUT_F32) {
                 if (out_row) *(f32x4*)((float*)out_row + 4 * c) = f32x4{y[0], y[1], y[2], y[3]};
             } else {
