@@ -29,6 +29,27 @@ def test_headers_declare_the_boundary():
         assert required in names
 
 
+def test_headers_are_plain_c(tmp_path):
+    """The boundary is a C ABI: both headers compile as strict C99 (and as
+    C++), and every declared function can be named from C."""
+    import shutil
+    import subprocess
+
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "boundary.c"
+    refs = "\n".join("    (void (*)(void))%s," % n for n in _declared())
+    src.write_text('#include "pipeboost.h"\n#include "pipeboost_ops.h"\n'
+                   "void (*boundary_functions[])(void) = {\n%s\n};\n" % refs)
+    inc = os.path.join(ROOT, "include")
+    for lang in (["-std=c99"], ["-x", "c++", "-std=c++11"]):
+        r = subprocess.run([cc] + lang + ["-Wall", "-Wextra", "-pedantic", "-Werror",
+                                          "-c", "-I" + inc, str(src), "-o", str(tmp_path / "b.o")],
+                           capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
+
+
 @pytest.mark.parametrize("name", _declared())
 def test_library_exports_declared_symbol(name):
     from paper_2503_17707_amd import binding as pb
