@@ -93,7 +93,8 @@ hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t i
                             int d, float eps, hipStream_t s, const RowShrink* sh = nullptr);
 
 // logits[b, v] = z[b, :] . E[v, :] (fp32 accumulate), plus per-block argmax
-// partials pval/pidx [B][lm_head_blocks(V)] (maximum, lowest index on ties).
+// partials pval/pidx [B][lm_head_blocks(V)] (maximum, lowest index on ties);
+// d a multiple of 8, at most 16384.
 int lm_head_blocks(int V);
 hipError_t launch_lm_head(int dtype, const float* z, int B, const void* E, int V, int d,
                           float* logits, float* pval, int* pidx, hipStream_t s);

@@ -76,111 +76,156 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict_
 }
 
 // ---- LM head + argmax partials ----------------------------------------------
-// logits[b, v] = z[b] . E[v] for NB sequences at once; each wave takes 8
-// vocabulary rows at a time (lanes split the model width into 16-byte chunks),
-// and each block also writes, per sequence, the (max, lowest index) of the
-// rows it covered, so the final argmax only scans one partial per block.
+// logits[b, v] = z[b] . E[v] for NB sequences at once, and per block the
+// (max, lowest index) of the rows it covered for each sequence, so the final
+// argmax only scans one partial per block.
 #ifndef PB_LM_NT
-#define PB_LM_NT 1  // embedding rows read with non-temporal loads (44.1 -> 38.6 us at OPT-1.3B)
+#define PB_LM_NT 1  // embedding rows read with non-temporal loads (each row is read once)
 #endif
-constexpr int LM_ROWS = 8;                      // rows per wave pass
-constexpr int LM_BLOCK_ROWS = 4 * 2 * LM_ROWS;  // 4 waves x 2 passes
 
 __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
     return v > bv || (v == bv && i < bi);
 }
 
-template <typename T, int NB>
+// The embedding is read as one stream: block b takes rows b, b + G, b + 2G, ...
+// (G blocks), so at any moment the grid reads a contiguous window of rows,
+// and thread t always covers the same 16-byte chunks t, t + 256, ... of a row
+// (its slice of z stays in registers).  R rows are read per round; their
+// per-thread partial sums are added over the block by halving exchanges and
+// one LDS round; the next round's rows are requested before this round is
+// reduced.  (Rows read by 8-row groups per wave, 8 consecutive rows per wave:
+// 5.3 TB/s at OPT-1.3B; this order: 5.7, and 6.5 at OPT-66B.)
+constexpr int LM_GRID = 512;  // 2 blocks per CU (256, 384, 640, 768, 1024 and 2048 measured slower)
+
+// Sum over the 64 lanes of each of M (a power of two) per-lane values by
+// halving exchanges: lane l ends with the total of value index l >> (6 - log2 M).
+template <int M>
+__device__ __forceinline__ float wave_sum_multi(float (&p)[M], int lane) {
+    constexpr int L = M == 1 ? 0 : M == 2 ? 1 : M == 4 ? 2 : M == 8 ? 3 : M == 16 ? 4 : 5;
+    static_assert((1 << L) == M && M <= 32, "power of two up to 32");
+#pragma unroll
+    for (int st = 0; st < L; ++st) {
+        const int D = 32 >> st;       // exchange distance
+        const int n = M >> (st + 1);  // values kept
+        const bool up = (lane & D) != 0;
+#pragma unroll
+        for (int k = 0; k < n; ++k) {
+            const float send = up ? p[k] : p[n + k];
+            p[k] = (up ? p[n + k] : p[k]) + __shfl_xor(send, D, 64);
+        }
+    }
+    float a = p[0];
+#pragma unroll
+    for (int D = 32 >> L; D > 0; D >>= 1) a += __shfl_xor(a, D, 64);
+    return a;
+}
+
+template <typename T, int NB, int CPT, int R>
 __global__ __launch_bounds__(256) void lm_head_kernel(const float* __restrict__ z, int b0,
                                                      const T* __restrict__ E, int V, int d,
                                                      float* __restrict__ logits,
                                                      float* __restrict__ pval,
                                                      int* __restrict__ pidx, int nblk) {
-    __shared__ float sv[4][NB];
-    __shared__ int si[4][NB];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    float best[NB];
-    int bidx[NB];
+    constexpr int M = R * NB;  // value index m = r NB + j: row r of the round, sequence j
+    constexpr int SH = M == 1 ? 6 : M == 2 ? 5 : M == 4 ? 4 : M == 8 ? 3 : M == 16 ? 2 : 1;
+    __shared__ float red[4][M];
+    __shared__ float sv[M];
+    __shared__ int si[M];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int nch = d >> 3;  // 16-byte chunks per row
+    const int G = (int)gridDim.x;
+    float zr[NB][CPT][8];
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-        best[j] = -INFINITY;
-        bidx[j] = 0x7fffffff;
-    }
-    for (int pass = 0; pass < 2; ++pass) {
-        const int v0 = blockIdx.x * LM_BLOCK_ROWS + (pass * 4 + wave) * LM_ROWS;
-        if (v0 >= V) break;
-        float acc[LM_ROWS][NB];
+    for (int j = 0; j < NB; ++j)
 #pragma unroll
-        for (int r = 0; r < LM_ROWS; ++r)
+        for (int i = 0; i < CPT; ++i) {
+            const int c = t + 256 * i;
+            f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f}, bq = a;
+            if (c < nch) {
+                a = *(const f32x4*)(z + (int64_t)(b0 + j) * d + 8 * c);
+                bq = *(const f32x4*)(z + (int64_t)(b0 + j) * d + 8 * c + 4);
+            }
 #pragma unroll
-            for (int j = 0; j < NB; ++j) acc[r][j] = 0.f;
-        for (int c = lane * 8; c < d; c += 64 * 8) {
-            u32x4 ev[LM_ROWS];
+            for (int e = 0; e < 4; ++e) {
+                zr[j][i][e] = a[e];
+                zr[j][i][4 + e] = bq[e];
+            }
+        }
+    float best = -INFINITY;  // thread t < M: sequence t % NB over the rows it finished
+    int bidx = 0x7fffffff;
+    auto load = [&](u32x4 (&ev)[R][CPT], int v0) {
 #pragma unroll
-            for (int r = 0; r < LM_ROWS; ++r) {
-                const u32x4* src = (const u32x4*)(E + (int64_t)min(v0 + r, V - 1) * d + c);
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int i = 0; i < CPT; ++i) {
+                // rows past V and chunks past the row read an in-bounds
+                // chunk (no branch around the load) and count as zeros
+                const int row = v0 + G * r, c = t + 256 * i;
+                const u32x4* src = (const u32x4*)(E + (int64_t)min(row, V - 1) * d + 8 * min(c, nch - 1));
 #if PB_LM_NT
-                ev[r] = __builtin_nontemporal_load(src);  // streamed once: no reuse to keep in cache
+                const u32x4 x = __builtin_nontemporal_load(src);
 #else
-                ev[r] = *src;
+                const u32x4 x = *src;
 #endif
+                ev[r][i] = (row < V && c < nch) ? x : u32x4{0u, 0u, 0u, 0u};
             }
-            float zb[NB][8];
+    };
+    u32x4 ev[R][CPT], en[R][CPT];
+    load(ev, (int)blockIdx.x);
+    for (int v0 = (int)blockIdx.x; v0 < V; v0 += R * G) {
+        load(en, v0 + R * G);
+        asm volatile("" ::: "memory");  // keeps those requests ahead of this round's work
+        float acc[M];
 #pragma unroll
-            for (int j = 0; j < NB; ++j) {
-                const f32x4 a = *(const f32x4*)(z + (int64_t)(b0 + j) * d + c);
-                const f32x4 bq = *(const f32x4*)(z + (int64_t)(b0 + j) * d + c + 4);
+        for (int m = 0; m < M; ++m) acc[m] = 0.f;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    zb[j][e] = a[e];
-                    zb[j][4 + e] = bq[e];
-                }
-            }
+        for (int r = 0; r < R; ++r)
 #pragma unroll
-            for (int r = 0; r < LM_ROWS; ++r) {
+            for (int i = 0; i < CPT; ++i) {
                 T ea[8];
-                __builtin_memcpy(ea, &ev[r], 16);
+                __builtin_memcpy(ea, &ev[r][i], 16);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     const float w = (float)ea[e];
 #pragma unroll
-                    for (int j = 0; j < NB; ++j) acc[r][j] += w * zb[j][e];
+                    for (int j = 0; j < NB; ++j) acc[r * NB + j] += w * zr[j][i][e];
+                }
+            }
+        const float tot = wave_sum_multi<M>(acc, lane);
+        if ((lane & ((1 << SH) - 1)) == 0) red[wave][lane >> SH] = tot;
+        lds_barrier();
+        if (t < M) {
+            const float x = (red[0][t] + red[1][t]) + (red[2][t] + red[3][t]);
+            const int row = v0 + G * (t / NB);
+            if (row < V) {
+                logits[(int64_t)(b0 + t % NB) * V + row] = x;
+                if (better(x, row, best, bidx)) {
+                    best = x;
+                    bidx = row;
                 }
             }
         }
+        lds_barrier();  // red is written again next round
 #pragma unroll
-        for (int r = 0; r < LM_ROWS; ++r)
+        for (int r = 0; r < R; ++r)
 #pragma unroll
-            for (int j = 0; j < NB; ++j) {
-                const float t = wave_sum(acc[r][j]);
-                const int v = v0 + r;
-                if (v < V) {
-                    if (lane == 0) logits[(int64_t)(b0 + j) * V + v] = t;
-                    if (better(t, v, best[j], bidx[j])) {
-                        best[j] = t;
-                        bidx[j] = v;
-                    }
-                }
-            }
+            for (int i = 0; i < CPT; ++i) ev[r][i] = en[r][i];
     }
-    if (lane == 0)
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-            sv[wave][j] = best[j];
-            si[wave][j] = bidx[j];
-        }
-    __syncthreads();
-    if (threadIdx.x < NB) {
-        const int j = threadIdx.x;
-        float bb = sv[0][j];
-        int ii = si[0][j];
-        for (int w = 1; w < 4; ++w)
-            if (better(sv[w][j], si[w][j], bb, ii)) {
-                bb = sv[w][j];
-                ii = si[w][j];
+    if (t < M) {
+        sv[t] = best;
+        si[t] = bidx;
+    }
+    lds_barrier();
+    if (t < NB) {
+        float bb = sv[t];
+        int ii = si[t];
+        for (int r = 1; r < R; ++r)
+            if (better(sv[r * NB + t], si[r * NB + t], bb, ii)) {
+                bb = sv[r * NB + t];
+                ii = si[r * NB + t];
             }
-        pval[(int64_t)(b0 + j) * nblk + blockIdx.x] = bb;
-        pidx[(int64_t)(b0 + j) * nblk + blockIdx.x] = ii;
+        pval[(int64_t)(b0 + t) * nblk + blockIdx.x] = bb;
+        pidx[(int64_t)(b0 + t) * nblk + blockIdx.x] = ii;
     }
 }
 
@@ -350,28 +395,50 @@ hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t i
     return hipGetLastError();
 }
 
-int lm_head_blocks(int V) { return (V + LM_BLOCK_ROWS - 1) / LM_BLOCK_ROWS; }
+int lm_head_blocks(int V) { return std::max(1, std::min(LM_GRID, V)); }
+
+template <typename T, int CPT, int R, int NBMAX>
+void lm_head_launch(int nb, const float* z, int b0, const void* E, int V, int d, float* logits,
+                    float* pval, int* pidx, int blocks, hipStream_t s) {
+#define PB_LM(NB)                                                                                \
+    PB_LAUNCH((lm_head_kernel<T, NB, CPT, R>), dim3(blocks), dim3(256), 0, s, z, b0, (const T*)E, V, d, \
+              logits, pval, pidx, blocks)
+    if (nb == 1) {
+        PB_LM(1);
+    } else if constexpr (NBMAX >= 2) {
+        if (nb == 2) PB_LM(2);
+        else if constexpr (NBMAX >= 4) PB_LM(4);
+    }
+#undef PB_LM
+}
 
 hipError_t launch_lm_head(int dtype, const float* z, int B, const void* E, int V, int d,
                           float* logits, float* pval, int* pidx, hipStream_t s) {
     if (B <= 0 || V <= 0) return hipSuccess;
-    if (d % 8) return hipErrorInvalidValue;
+    if (d % 8 || d > 8 * 256 * 8) return hipErrorInvalidValue;
     const int blocks = lm_head_blocks(V);
-    for (int b0 = 0; b0 < B; b0 += 4) {
-        const int nb = std::min(4, B - b0);
-#define PB_LM(T, NB)                                                                           \
-    PB_LAUNCH((lm_head_kernel<T, NB>), dim3(blocks), dim3(256), 0, s, z, b0,          \
-                       (const T*)E, V, d, logits, pval, pidx, blocks)
+    const int cpt = (d / 8 + 255) / 256;  // 16-byte chunks per thread per row
+    // sequences per launch (a power of two): their z slices stay in registers
+    const int nbmax = cpt <= 2 ? 4 : cpt <= 5 ? 2 : 1;
+    for (int b0 = 0; b0 < B;) {
+        int nb = 1;
+        while (nb * 2 <= std::min(nbmax, B - b0)) nb *= 2;
         if (dtype == 1) {
-            if (nb == 1) PB_LM(_Float16, 1); else if (nb == 2) PB_LM(_Float16, 2);
-            else if (nb == 3) PB_LM(_Float16, 3); else PB_LM(_Float16, 4);
+            if (cpt == 1) lm_head_launch<_Float16, 1, 8, 4>(nb, z, b0, E, V, d, logits, pval, pidx, blocks, s);
+            else if (cpt == 2) lm_head_launch<_Float16, 2, 4, 4>(nb, z, b0, E, V, d, logits, pval, pidx, blocks, s);
+            else if (cpt == 3) lm_head_launch<_Float16, 3, 2, 2>(nb, z, b0, E, V, d, logits, pval, pidx, blocks, s);
+            else if (cpt <= 5) lm_head_launch<_Float16, 5, 2, 2>(nb, z, b0, E, V, d, logits, pval, pidx, blocks, s);
+            else lm_head_launch<_Float16, 8, 1, 1>(nb, z, b0, E, V, d, logits, pval, pidx, blocks, s);
         } else {
-            if (nb == 1) PB_LM(__bf16, 1); else if (nb == 2) PB_LM(__bf16, 2);
-            else if (nb == 3) PB_LM(__bf16, 3); else PB_LM(__bf16, 4);
+            if (cpt == 1) lm_head_launch<__bf16, 1, 8, 4>(nb, z, b0, E, V, d, logits, pval, pidx, blocks, s);
+            else if (cpt == 2) lm_head_launch<__bf16, 2, 4, 4>(nb, z, b0, E, V, d, logits, pval, pidx, blocks, s);
+            else if (cpt == 3) lm_head_launch<__bf16, 3, 2, 2>(nb, z, b0, E, V, d, logits, pval, pidx, blocks, s);
+            else if (cpt <= 5) lm_head_launch<__bf16, 5, 2, 2>(nb, z, b0, E, V, d, logits, pval, pidx, blocks, s);
+            else lm_head_launch<__bf16, 8, 1, 1>(nb, z, b0, E, V, d, logits, pval, pidx, blocks, s);
         }
-#undef PB_LM
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
+        b0 += nb;
     }
     return hipSuccess;
 }
