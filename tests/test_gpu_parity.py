@@ -40,6 +40,13 @@ SMALL = {
                                 d_ffn=256, vocab=500, max_pos=8, dtype="f16", batch=4, seq_len=1,
                                 lora_targets=("q", "v"), lora_rank=4, lora_alpha=8.0,
                                 n_adapters=0),
+    # the widest model the library accepts (d_model 16384, 128 heads of 128):
+    # LayerNorm rows of 16 chunks per thread, the LM head's widest rows (one
+    # sequence per launch, three launches), K = 16384 GEMM tiles
+    "widest": synth.Workload(name="widest", seed=39, n_layers=1, d_model=16384, n_heads=128,
+                             d_ffn=256, vocab=600, max_pos=16, dtype="f16", batch=3, seq_len=9,
+                             lora_targets=("q", "v"), lora_rank=4, lora_alpha=8.0, n_adapters=1,
+                             adapter_of_seq=(0, -1, 0)),
 }
 
 
