@@ -40,6 +40,12 @@ SMALL = {
                                 d_ffn=256, vocab=500, max_pos=8, dtype="f16", batch=4, seq_len=1,
                                 lora_targets=("q", "v"), lora_rank=4, lora_alpha=8.0,
                                 n_adapters=0),
+    # the largest LoRA rank the library accepts (64), two adapters on all four
+    # projections: 128 packed columns, four 16-rank groups per row shrink
+    "rank64": synth.Workload(name="rank64", seed=40, n_layers=2, d_model=256, n_heads=4, d_ffn=512,
+                             vocab=700, max_pos=64, dtype="bf16", batch=3, seq_len=40,
+                             lora_targets=("q", "k", "v", "o"), lora_rank=64, lora_alpha=128.0,
+                             n_adapters=2, adapter_of_seq=(1, 0, -1)),
     # the widest model the library accepts (d_model 16384, 128 heads of 128):
     # LayerNorm rows of 16 chunks per thread, the LM head's widest rows (one
     # sequence per launch, three launches), K = 16384 GEMM tiles
