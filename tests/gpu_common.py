@@ -16,7 +16,7 @@ def log(*a):
     sys.stdout.flush()
 
 
-def compare(tag, got_logits, got_tok, ref_logits, ref_tok):
+def compare(tag, got_logits, got_tok, ref_logits, ref_tok, max_abs=MAX_ABS):
     ref = np.asarray(ref_logits, dtype=np.float64)
     got = np.asarray(got_logits, dtype=np.float64)
     assert got.shape == ref.shape, (got.shape, ref.shape)
@@ -31,7 +31,7 @@ def compare(tag, got_logits, got_tok, ref_logits, ref_tok):
     log("%s: max|d|=%.3e rel_l2 per sequence=%s tokens gpu=%s oracle=%s margin=%s" % (
         tag, maxd, np.array2string(rows, precision=3), list(got_tok), list(ref_tok),
         np.round(margin, 4).tolist()))
-    assert maxd <= MAX_ABS, "%s: max|d| %.3e > %.1e" % (tag, maxd, MAX_ABS)
+    assert maxd <= max_abs, "%s: max|d| %.3e > %.3e" % (tag, maxd, max_abs)
     assert rel <= MAX_REL_L2, "%s: rel L2 %.3e > %.1e" % (tag, rel, MAX_REL_L2)
     assert list(got_tok) == list(ref_tok), "%s: greedy tokens differ (margins %s)" % (tag, margin)
     return maxd, rel
