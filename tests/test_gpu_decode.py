@@ -26,6 +26,12 @@ CASES = {
     "long64": synth.Workload(name="long64", seed=33, n_layers=2, d_model=128, n_heads=2, d_ffn=256,
                              vocab=500, max_pos=1040, dtype="f16", batch=1, seq_len=1030,
                              lora_targets=("q", "k", "v", "o"), lora_rank=8, lora_alpha=8.0, n_adapters=1),
+    # six sequences: the GEMVs' widest row group (8 token rows, two of them
+    # clamped), three adapters and the base mixed, bf16
+    "batch6": synth.Workload(name="batch6", seed=35, n_layers=2, d_model=256, n_heads=4, d_ffn=512,
+                             vocab=800, max_pos=64, dtype="bf16", batch=6, seq_len=21,
+                             lora_targets=("q", "k", "v", "o"), lora_rank=8, lora_alpha=16.0,
+                             n_adapters=3, adapter_of_seq=(0, 1, -1, 2, 0, -1)),
 }
 STEPS = 4
 

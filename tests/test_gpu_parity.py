@@ -41,6 +41,12 @@ SMALL = {
                                 d_ffn=256, vocab=500, max_pos=8, dtype="f16", batch=4, seq_len=1,
                                 lora_targets=("q", "v"), lora_rank=4, lora_alpha=8.0,
                                 n_adapters=0),
+    # eight one-token sequences: every product of the prefill takes the GEMV
+    # path with its widest row group (8 rows), adapters mixed on all four
+    "eight_tokens": synth.Workload(name="eight_tokens", seed=36, n_layers=2, d_model=256, n_heads=4,
+                                   d_ffn=512, vocab=600, max_pos=8, dtype="f16", batch=8, seq_len=1,
+                                   lora_targets=("q", "k", "v", "o"), lora_rank=8, lora_alpha=16.0,
+                                   n_adapters=2, adapter_of_seq=(0, -1, 1, 1, 0, -1, -1, 0)),
     # the largest LoRA rank the library accepts (64), two adapters on all four
     # projections: 128 packed columns, four 16-rank groups per row shrink
     "rank64": synth.Workload(name="rank64", seed=40, n_layers=2, d_model=256, n_heads=4, d_ffn=512,
