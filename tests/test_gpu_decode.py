@@ -26,6 +26,11 @@ CASES = {
     "long64": synth.Workload(name="long64", seed=33, n_layers=2, d_model=128, n_heads=2, d_ffn=256,
                              vocab=500, max_pos=1040, dtype="f16", batch=1, seq_len=1030,
                              lora_targets=("q", "k", "v", "o"), lora_rank=8, lora_alpha=8.0, n_adapters=1),
+    # f16 with head_dim 128 (the OPT-6.7B to 66B head size and storage type)
+    "f16_hd128": synth.Workload(name="f16_hd128", seed=38, n_layers=2, d_model=256, n_heads=2, d_ffn=384,
+                                vocab=700, max_pos=96, dtype="f16", batch=2, seq_len=70,
+                                lora_targets=("q", "v"), lora_rank=16, lora_alpha=32.0, n_adapters=1,
+                                adapter_of_seq=(0, -1)),
     # six sequences: the GEMVs' widest row group (8 token rows, two of them
     # clamped), three adapters and the base mixed, bf16
     "batch6": synth.Workload(name="batch6", seed=35, n_layers=2, d_model=256, n_heads=4, d_ffn=512,
