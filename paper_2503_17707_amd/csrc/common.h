@@ -40,30 +40,16 @@ template <typename T> __device__ inline typename Mfma<T>::vec8 as_vec8(u32x4 v) 
     return __builtin_bit_cast(typename Mfma<T>::vec8, v);
 }
 
-// One 16-byte global -> LDS copy per lane (LDS-DMA, global_load_lds_dwordx4):
-// lane i writes bytes [16 i, 16 i + 16) after the wave-uniform LDS address
-// lds_base.  Issued from inline assembly so that the compiler, which would
-// otherwise drain every outstanding load before the next LDS read, leaves the
-// waiting to explicit s_waitcnt (wait_vmcnt); later compiler-placed waits only
-// ever wait for more, never less.  M0 is saved and restored around the copy,
-// so the compiler's own use of M0 is never disturbed, and one wait state
+// One 16-byte global -> LDS copy per lane (LDS-DMA, global_load_lds_dwordx4)
+// from a wave-uniform 64-bit base (SGPRs) plus a 32-bit per-lane byte offset
+// (voffset, saddr form: each lane's address costs one 32-bit offset): lane i
+// writes bytes [16 i, 16 i + 16) after the wave-uniform LDS address lds_base.
+// Issued from inline assembly so that the compiler, which would otherwise
+// drain every outstanding load before the next LDS read, leaves the waiting
+// to explicit s_waitcnt (wait_vmcnt); later compiler-placed waits only ever
+// wait for more, never less.  M0 is saved and restored around the copy, so
+// the compiler's own use of M0 is never disturbed, and one wait state
 // separates the M0 write from the copy that reads it.
-__device__ __forceinline__ void dma16(const void* gptr, uint32_t lds_base) {
-    uint32_t saved;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\t"
-        "s_mov_b32 m0, %1\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %2, off\n\t"
-        "s_mov_b32 m0, %0"
-        : "=&s"(saved)
-        : "s"(lds_base), "v"(gptr)
-        : "memory");
-}
-
-// The same copy with a wave-uniform 64-bit base (SGPRs) and a 32-bit
-// per-lane byte offset (global_load_lds_dwordx4 voffset, saddr): the base
-// stays scalar and each lane's address costs one 32-bit offset.
 __device__ __forceinline__ void dma16s(const void* sbase, uint32_t voff, uint32_t lds_base) {
     uint32_t saved;
     asm volatile(

@@ -42,10 +42,18 @@ __global__ __launch_bounds__(256) void embed_kernel(const int32_t* __restrict__ 
 
 // ---- LayerNorm: one 256-thread block per row, values kept in registers ------
 constexpr int LN_MAXC = 16;  // float4 chunks per thread: d <= 256 * 4 * 16
+#ifndef PB_LN_FEW_G
+#define PB_LN_FEW_G 4  // ranks per shrink block of a launch with few rows
+#endif
+#ifndef PB_LN_AHEAD
+#define PB_LN_AHEAD 1  // ... whose slot and first A rows are requested before the LayerNorm
+#endif
 
 // SHRINK: the row's LoRA shrink rides along (compiled only where it is used,
-// since its registers would lower the occupancy of the plain kernel)
-template <typename T, bool OUT_F32, int MAXC, bool SHRINK>
+// since its registers would lower the occupancy of the plain kernel), in
+// groups of G ranks; AHEAD: the slot and the block's first group of A rows
+// are requested before the row's LayerNorm (launches of few rows)
+template <typename T, bool OUT_F32, int MAXC, bool SHRINK, int G, bool AHEAD>
 __global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict__ x,
                                                        int64_t in_mul, int64_t in_add,
                                                        const T* __restrict__ g,
@@ -55,15 +63,21 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict_
     const int row = blockIdx.x;
     const float* xr = x + ((int64_t)row * in_mul + in_add) * d;
     const int nc = d / 4;
+    constexpr bool PRE = SHRINK && AHEAD && !OUT_F32;
+    const int slot = PRE ? sh.row_slot[row] : -1;
     f32x4 v[MAXC];
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i) {
+        const int c = threadIdx.x + 256 * i;
+        if (c < nc) v[i] = *(const f32x4*)(xr + 4 * c);
+    }
+    ShrinkAhead<MAXC, G> ahead;
+    if (PRE) shrink_ahead<T, MAXC, G>(sh, d, slot, (int)blockIdx.y, (int)gridDim.y, ahead);
     float s = 0.f;
 #pragma unroll
     for (int i = 0; i < MAXC; ++i) {
         const int c = threadIdx.x + 256 * i;
-        if (c < nc) {
-            v[i] = *(const f32x4*)(xr + 4 * c);
-            s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
-        }
+        if (c < nc) s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
     }
     // with gridDim.y > 1 every block of the row normalizes it, block 0 writes
     // it, and the blocks share the row's LoRA shrink
@@ -71,7 +85,7 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const float* __restrict_
     row_layernorm<T, MAXC, OUT_F32>(v, s, nc, g, b, blockIdx.y == 0 ? orow : nullptr, eps, red);
     if (!OUT_F32 && SHRINK) {
         __shared__ float red16[4][16];
-        row_shrink<T, MAXC>(sh, row, d, v, red16, (int)blockIdx.y, (int)gridDim.y);
+        row_shrink<T, MAXC, G>(sh, row, d, v, red16, (int)blockIdx.y, (int)gridDim.y, PRE ? &ahead : nullptr);
     }
 }
 
@@ -98,9 +112,12 @@ __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
 constexpr int LM_GRID = 512;  // 2 blocks per CU (256, 384, 640, 768, 1024 and 2048 measured slower)
 
 // Sum over the 64 lanes of each of M (a power of two) per-lane values by
-// halving exchanges: lane l ends with the total of value index l >> (6 - log2 M).
+// halving exchanges in place: lane l ends with the total of value index
+// l >> (6 - log2 M), the same exchanges and sums as wave_sum_multi.  The LM
+// head keeps this form: its loop measured 35.1-35.5 us at OPT-1.3B against
+// 37.2-37.7 with the fresh-array form, which needs fewer registers.
 template <int M>
-__device__ __forceinline__ float wave_sum_multi(float (&p)[M], int lane) {
+__device__ __forceinline__ float wave_sum_inplace(float (&p)[M], int lane) {
     constexpr int L = M == 1 ? 0 : M == 2 ? 1 : M == 4 ? 2 : M == 8 ? 3 : M == 16 ? 4 : 5;
     static_assert((1 << L) == M && M <= 32, "power of two up to 32");
 #pragma unroll
@@ -191,7 +208,7 @@ __global__ __launch_bounds__(256) void lm_head_kernel(const float* __restrict__ 
                     for (int j = 0; j < NB; ++j) acc[r * NB + j] += w * zr[j][i][e];
                 }
             }
-        const float tot = wave_sum_multi<M>(acc, lane);
+        const float tot = wave_sum_inplace<M>(acc, lane);
         if ((lane & ((1 << SH) - 1)) == 0) red[wave][lane >> SH] = tot;
         lds_barrier();
         if (t < M) {
@@ -359,18 +376,23 @@ hipError_t launch_layernorm(int dtype, const float* x, int64_t in_mul, int64_t i
     if (d % 4 || d > 256 * 4 * LN_MAXC) return hipErrorInvalidValue;
     RowShrink sh{};
     if (shp && !out_f32) sh = *shp;
-    // a few rows (decode steps): the row's shrink groups of 16 ranks go to
-    // blocks of their own, so that the A reads spread over several CUs
+    // a few rows (decode steps): the row's shrink groups of PB_LN_FEW_G ranks
+    // go to blocks of their own, so that the A reads spread over several CUs
+    // (many rows: groups of 16, one block per row)
+    const bool few = sh.Acat && rows <= 8;
     int slices = 1;
-    if (sh.Acat && rows <= 8)
-        slices = std::max(1, __builtin_popcount(sh.mask & 7u) * ((sh.rs + 15) / 16));
-#define PB_LN2(T, F, C, SH)                                                                        \
-    PB_LAUNCH((layernorm_kernel<T, F, C, SH>), dim3(rows, slices), dim3(256), 0, s, x, in_mul,      \
+    if (few) slices = std::max(1, __builtin_popcount(sh.mask & 7u) * ((sh.rs + PB_LN_FEW_G - 1) / PB_LN_FEW_G));
+#define PB_LN2(T, F, C, SH, G, AH)                                                                 \
+    PB_LAUNCH((layernorm_kernel<T, F, C, SH, G, AH>), dim3(rows, slices), dim3(256), 0, s, x, in_mul, \
               in_add, (const T*)g, (const T*)b, out, d, eps, sh)
 #define PB_LN1(T, F, C)                                                                            \
     do {                                                                                           \
-        if (!F && sh.Acat) PB_LN2(T, false, C, true);                                              \
-        else PB_LN2(T, F, C, false);                                                               \
+        if (!F && sh.Acat) {                                                                       \
+            if (few) PB_LN2(T, false, C, true, PB_LN_FEW_G, PB_LN_AHEAD);                          \
+            else PB_LN2(T, false, C, true, 16, false);                                             \
+        } else {                                                                                   \
+            PB_LN2(T, F, C, false, 16, false);                                                     \
+        }                                                                                          \
     } while (0)
     // chunks per thread fitted to d: registers decide how many rows a CU
     // keeps in flight, and the kernel is bound by the latency of its rows

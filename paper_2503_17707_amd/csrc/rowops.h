@@ -109,48 +109,110 @@ __device__ __forceinline__ void row_layernorm(f32x4 (&v)[MAXC], float sum, int n
     }
 }
 
-// Sum of each of 16 per-lane values over the 64 lanes of a wave, by halving
-// exchanges: afterwards lane l holds the total of value index
-// 8 b5 + 4 b4 + 2 b3 + b2 (b_k = bit k of l).  17 exchanges instead of 96.
-__device__ __forceinline__ float wave_sum16(const float (&p)[16], int lane) {
-    const bool h5 = (lane >> 5) & 1, h4 = (lane >> 4) & 1, h3 = (lane >> 3) & 1, h2 = (lane >> 2) & 1;
-    float a8[8], a4[4], a2[2];
+// Sum over the 64 lanes of each of M (a power of two up to 32) per-lane
+// values by halving exchanges: afterwards lane l holds the total of value
+// index l >> (6 - log2 M) (for M = 16: 8 b5 + 4 b4 + 2 b3 + b2, b_k = bit k
+// of l); M - 1 + 6 - log2 M exchanges instead of 6 M.  Each step keeps the
+// half it still needs in a fresh array, so the values already exchanged are
+// dead (fewer live registers than halving in place).
+template <int M, int D>
+__device__ __forceinline__ float wave_sum_halves(const float (&p)[M], int lane) {
+    if constexpr (M == 1) {
+        float a = p[0];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-        const float send = h5 ? p[k] : p[8 + k];
-        a8[k] = (h5 ? p[8 + k] : p[k]) + __shfl_xor(send, 32, 64);
-    }
+        for (int e = D; e > 0; e >>= 1) a += __shfl_xor(a, e, 64);
+        return a;
+    } else {
+        constexpr int n = M / 2;
+        const bool up = (lane & D) != 0;
+        float q[n];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const float send = h4 ? a8[k] : a8[4 + k];
-        a4[k] = (h4 ? a8[4 + k] : a8[k]) + __shfl_xor(send, 16, 64);
+        for (int k = 0; k < n; ++k) {
+            const float send = up ? p[k] : p[n + k];
+            q[k] = (up ? p[n + k] : p[k]) + __shfl_xor(send, D, 64);
+        }
+        return wave_sum_halves<n, D / 2>(q, lane);
     }
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-        const float send = h3 ? a4[k] : a4[2 + k];
-        a2[k] = (h3 ? a4[2 + k] : a4[k]) + __shfl_xor(send, 8, 64);
-    }
-    float a1 = (h2 ? a2[1] : a2[0]) + __shfl_xor(h2 ? a2[0] : a2[1], 4, 64);
-    a1 += __shfl_xor(a1, 2, 64);
-    a1 += __shfl_xor(a1, 1, 64);
-    return a1;
+}
+
+template <int M>
+__device__ __forceinline__ float wave_sum_multi(const float (&p)[M], int lane) {
+    static_assert(M >= 1 && M <= 32 && (M & (M - 1)) == 0, "power of two up to 32");
+    return wave_sum_halves<M, 32>(p, lane);
 }
 
 // u: this thread's values of the row, chunk i covers columns 4 (tid + 256 i) .. +3
 // (chunks past the row's end may hold anything).  Must be called by all 256
-// threads of the block (it synchronizes).  The loads of a chunk's 16 A rows
-// are unconditional (ranks past rs re-read row rs - 1 and are dropped) so that
-// they are in flight together.
+// threads of the block (it synchronizes).  Ranks go in groups of G (4, 8 or
+// 16); the loads of a chunk's G A rows are unconditional (ranks past rs
+// re-read row rs - 1 and are dropped) so that they are in flight together.
 //
 // With several blocks per row (slice of nslice), block `slice` takes every
-// nslice-th group of 16 ranks (targets in order) and only slice 0 writes the
+// nslice-th group of G ranks (targets in order) and only slice 0 writes the
 // zero columns.
-template <typename T, int MAXC>
+// The A words of the first rank group a block takes, with the row's slot and
+// scale, loaded before the row's LayerNorm so that their latency overlaps it (for
+// launches of few rows: it costs MAXC x G x 2 registers per thread).
+template <int MAXC, int G>
+struct ShrinkAhead {
+    int slot;            // the row's adapter slot (< 0: none)
+    float scale;         // its LoRA scale
+    int t, j0;           // the block's first group: target and first rank (t < 0: none)
+    u32x2 raw[MAXC][G];  // its A words at this thread's chunks
+};
+
+// Issue the loads of `a` (block `slice` of `nslice` on row m); `slot` is the
+// row's slot, loaded by the caller ahead of its own row loads.
+template <typename T, int MAXC, int G>
+__device__ __forceinline__ void shrink_ahead(const RowShrink& sh, int d, int slot, int slice, int nslice,
+                                             ShrinkAhead<MAXC, G>& a) {
+    a.slot = slot;
+    a.t = -1;
+    a.j0 = 0;
+    if (slot < 0) return;
+    a.scale = sh.slot_scale[slot];
+    int group = 0;  // groups in (target, first rank) order; the block's first is number `slice`
+    for (int t = 0; t < 3 && a.t < 0; ++t) {
+        if (!((sh.mask >> t) & 1u)) continue;
+        for (int j0 = 0; j0 < sh.rs; j0 += G)
+            if (group++ == slice) {
+                a.t = t;
+                a.j0 = j0;
+                break;
+            }
+    }
+    if (a.t < 0) return;  // uniform across the block
+    const T* A = (const T*)sh.Acat;
+    const int nc = d / 4;
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i) {
+        if (256 * i >= nc) break;  // uniform
+        const int c = threadIdx.x + 256 * i;
+        const int cc = c < nc ? c : 0;
+#pragma unroll
+        for (int o = 0; o < G; ++o)
+            a.raw[i][o] = *(const u32x2*)(A + (int64_t)(a.t * sh.kw + slot * sh.rs + min(a.j0 + o, sh.rs - 1)) * d +
+                                          4 * cc);
+    }
+}
+
+// u: this thread's values of the row, chunk i covers columns 4 (tid + 256 i) .. +3
+// (chunks past the row's end may hold anything).  Must be called by all 256
+// threads of the block (it synchronizes).  Ranks go in groups of G (4, 8 or
+// 16); the loads of a chunk's G A rows are unconditional (ranks past rs
+// re-read row rs - 1 and are dropped) so that they are in flight together.
+//
+// With several blocks per row (slice of nslice), block `slice` takes every
+// nslice-th group of G ranks (targets in order) and only slice 0 writes the
+// zero columns.  `ahead` (may be null): the slot, its scale and the first
+// group's A words, already loaded by shrink_ahead.
+template <typename T, int MAXC, int G = 16>
 __device__ __forceinline__ void row_shrink(const RowShrink& sh, int m, int d, const f32x4 (&u)[MAXC],
-                                           float (*red)[16], int slice = 0, int nslice = 1) {
+                                           float (*red)[16], int slice = 0, int nslice = 1,
+                                           const ShrinkAhead<MAXC, G>* ahead = nullptr) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int nc = d / 4;
-    const int slot = sh.row_slot[m];
+    const int slot = ahead ? ahead->slot : sh.row_slot[m];
     T* zr = (T*)sh.Z + (int64_t)m * 4 * sh.kw;
     // zero every column outside the row's own slot block of an active target
     if (slice == 0)
@@ -160,46 +222,48 @@ __device__ __forceinline__ void row_shrink(const RowShrink& sh, int m, int d, co
             if (!own) zr[c] = (T)0.f;
         }
     if (slot < 0) return;  // uniform across the block
-    const float scale = sh.slot_scale[slot];
+    const float scale = ahead ? ahead->scale : sh.slot_scale[slot];
     const T* A = (const T*)sh.Acat;
-    const int o_lane = 8 * ((lane >> 5) & 1) + 4 * ((lane >> 4) & 1) + 2 * ((lane >> 3) & 1) + ((lane >> 2) & 1);
+    static_assert(G == 4 || G == 8 || G == 16, "rank groups of 4, 8 or 16");
+    constexpr int LG = G == 4 ? 2 : G == 8 ? 3 : 4;
     int group = 0;
     for (int t = 0; t < 3; ++t) {
         if (!((sh.mask >> t) & 1u)) continue;
-        for (int j0 = 0; j0 < sh.rs; j0 += 16) {
+        for (int j0 = 0; j0 < sh.rs; j0 += G) {
             if (group++ % nslice != slice) continue;  // uniform across the block
-            const T* rows[16];
+            const bool pre = ahead && t == ahead->t && j0 == ahead->j0;  // uniform
+            const T* rows[G];
 #pragma unroll
-            for (int o = 0; o < 16; ++o)
+            for (int o = 0; o < G; ++o)
                 rows[o] = A + (int64_t)(t * sh.kw + slot * sh.rs + min(j0 + o, sh.rs - 1)) * d;
-            float part[16];
+            float part[G];
 #pragma unroll
-            for (int o = 0; o < 16; ++o) part[o] = 0.f;
+            for (int o = 0; o < G; ++o) part[o] = 0.f;
 #pragma unroll
             for (int i = 0; i < MAXC; ++i) {
                 if (256 * i >= nc) break;  // uniform
                 const int c = tid + 256 * i;
                 const bool valid = c < nc;
                 const int cc = valid ? c : 0;
-                u32x2 raw[16];
+                u32x2 raw[G];
 #pragma unroll
-                for (int o = 0; o < 16; ++o) raw[o] = *(const u32x2*)(rows[o] + 4 * cc);
+                for (int o = 0; o < G; ++o) raw[o] = pre ? ahead->raw[i][o] : *(const u32x2*)(rows[o] + 4 * cc);
                 float uu[4];
 #pragma unroll
                 for (int r = 0; r < 4; ++r) uu[r] = valid ? u[i][r] : 0.f;
 #pragma unroll
-                for (int o = 0; o < 16; ++o) {
+                for (int o = 0; o < G; ++o) {
                     T a4[4];
                     __builtin_memcpy(a4, &raw[o], 8);
                     part[o] += uu[0] * (float)a4[0] + uu[1] * (float)a4[1] + uu[2] * (float)a4[2] +
                                uu[3] * (float)a4[3];
                 }
             }
-            const float tot = wave_sum16(part, lane);
+            const float tot = wave_sum_multi<G>(part, lane);
             lds_barrier();  // previous use of red finished
-            if ((lane & 3) == 0) red[wave][o_lane] = tot;
+            if ((lane & ((64 >> LG) - 1)) == 0) red[wave][lane >> (6 - LG)] = tot;
             lds_barrier();
-            if (tid < 16 && j0 + tid < sh.rs) {
+            if (tid < G && j0 + tid < sh.rs) {
                 const float zsum = (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
                 zr[t * sh.kw + slot * sh.rs + j0 + tid] = (T)(scale * zsum);
             }
