@@ -31,6 +31,12 @@ CASES = {
                                 vocab=700, max_pos=96, dtype="f16", batch=2, seq_len=70,
                                 lora_targets=("q", "v"), lora_rank=16, lora_alpha=32.0, n_adapters=1,
                                 adapter_of_seq=(0, -1)),
+    # the largest rank (64) on q, k, v, o with two adapters: the decode
+    # LayerNorm's shrink spread over 48 blocks of 4 ranks per row
+    "rank64": synth.Workload(name="rank64", seed=40, n_layers=2, d_model=256, n_heads=4, d_ffn=512,
+                             vocab=700, max_pos=48, dtype="bf16", batch=3, seq_len=24,
+                             lora_targets=("q", "k", "v", "o"), lora_rank=64, lora_alpha=128.0,
+                             n_adapters=2, adapter_of_seq=(1, 0, -1)),
     # six sequences: the GEMVs' widest row group (8 token rows, two of them
     # clamped), three adapters and the base mixed, bf16
     "batch6": synth.Workload(name="batch6", seed=35, n_layers=2, d_model=256, n_heads=4, d_ffn=512,
